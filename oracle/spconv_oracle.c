@@ -1,0 +1,182 @@
+/*
+ * Plain CPU oracle for the fused sparse direct convolution.
+ *
+ * TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the benchmark's
+ * CPU-baseline leg may load or call this code. It shares nothing with the GPU
+ * library: no headers, no helpers, no tables.
+ *
+ * What it computes (paper, "Optimizing Sparse Neural Networks", paragraph
+ * "Sparse Convolution with CSR", together with the dense convolution of
+ * "The Tiramisu Embedded DSL" and the Conv -> ReLU -> Maxpool block of the
+ * "Evaluation" section):
+ *
+ *   pre[n,k,y,x] = b[k] + sum over nonzero taps (c,r,s) of row k of
+ *                  W[k,c,r,s] * Xpad[n, c, y*stride + r, x*stride + s]
+ *   o            = relu ? max(pre, 0) : pre
+ *   out          = pool ? max over a,b in {0,1} of o[n,k,2i+a,2j+b] : o
+ *
+ * Xpad is X surrounded by `pad` zeros; here the zero border is expressed as a
+ * bounds test on the unpadded X, so the oracle never builds a padded copy.
+ * Sums are taken in double precision, tap by tap in (c, r, s) order, which is
+ * the order the paper's CSR loop visits the nonzeros of one output channel.
+ * The oracle also returns, per output, the sum of |w * x| over the same terms
+ * (the max of it over the pooling window when pooling), which bounds the
+ * rounding error of any fp32 evaluation order.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* An entry is a nonzero of the sparse filter: with a mask, every position whose
+ * mask byte is nonzero (an explicit 0.0 value stays an entry); without one,
+ * every value that compares unequal to 0.0f (so -0.0 is dropped, NaN is kept). */
+static int oracle_is_entry(const float *w, const uint8_t *mask, size_t i) {
+    if (mask) return mask[i] != 0;
+    return w[i] != 0.0f;
+}
+
+/*
+ * CSR packing of the filter (paper, "Sparse Convolution with CSR"): the
+ * (K, C, R, S) tensor is viewed as a K x (C*R*S) matrix whose column is the
+ * flattened tap (c, r, s); each row is compressed. Besides the column index,
+ * every entry carries the tap's offset inside one zero-padded input image of
+ * C planes of Hp x Wp, which is what the paper's loop adds to the output
+ * position: offset = c*Hp*Wp + r*Wp + s.
+ *
+ * rowptr has K+1 slots; colidx, offset and vals need room for K*C*R*S entries.
+ * Returns the number of entries.
+ */
+long long oracle_pack_csr(const float *w, const uint8_t *mask, int K, int C, int R, int S, int Hp, int Wp,
+                          int32_t *rowptr, int32_t *colidx, int32_t *offset, float *vals) {
+    long long nnz = 0;
+    rowptr[0] = 0;
+    for (int k = 0; k < K; ++k) {
+        for (int c = 0; c < C; ++c)
+            for (int r = 0; r < R; ++r)
+                for (int s = 0; s < S; ++s) {
+                    size_t i = (((size_t)k * C + c) * R + r) * S + s;
+                    if (!oracle_is_entry(w, mask, i)) continue;
+                    colidx[nnz] = (int32_t)((c * R + r) * S + s);
+                    offset[nnz] = (int32_t)(c * Hp * Wp + r * Wp + s);
+                    memcpy(&vals[nnz], &w[i], sizeof(float));
+                    ++nnz;
+                }
+        rowptr[k + 1] = (int32_t)nnz;
+    }
+    return nnz;
+}
+
+/* Output extent of the convolution (before pooling). */
+static int oracle_out_extent(int in, int f, int stride, int pad) {
+    return (in + 2 * pad - f) / stride + 1;
+}
+
+/* One output plane (n, k): sums, activation and pooling as described above. */
+static void oracle_plane(const float *x, int C, int H, int W, const float *w, const uint8_t *mask, int R, int S,
+                         const float *bias, int stride, int pad, int relu, int pool, int n, int k,
+                         double *acc, double *ab, double *out, double *absout) {
+    const int Ho = oracle_out_extent(H, R, stride, pad);
+    const int Wo = oracle_out_extent(W, S, stride, pad);
+    const double b = bias ? (double)bias[k] : 0.0;
+    for (int i = 0; i < Ho * Wo; ++i) {
+        acc[i] = b;
+        ab[i] = 0.0;
+    }
+    /* Walk the nonzeros of filter row k in (c, r, s) order. */
+    for (int c = 0; c < C; ++c)
+        for (int r = 0; r < R; ++r)
+            for (int s = 0; s < S; ++s) {
+                size_t wi = (((size_t)k * C + c) * R + r) * S + s;
+                if (!oracle_is_entry(w, mask, wi)) continue;
+                const double coeff = (double)w[wi];
+                const float *plane = x + ((size_t)n * C + c) * H * W;
+                for (int y = 0; y < Ho; ++y) {
+                    const int iy = y * stride + r - pad;
+                    for (int xo = 0; xo < Wo; ++xo) {
+                        const int ix = xo * stride + s - pad;
+                        double v = 0.0;
+                        if (iy >= 0 && iy < H && ix >= 0 && ix < W) v = (double)plane[(size_t)iy * W + ix];
+                        acc[y * Wo + xo] += coeff * v;
+                        ab[y * Wo + xo] += fabs(coeff * v);
+                    }
+                }
+            }
+    if (relu)
+        for (int i = 0; i < Ho * Wo; ++i) acc[i] = acc[i] > 0.0 ? acc[i] : 0.0;
+    if (!pool) {
+        memcpy(out, acc, sizeof(double) * Ho * Wo);
+        memcpy(absout, ab, sizeof(double) * Ho * Wo);
+        return;
+    }
+    const int Hq = Ho / 2, Wq = Wo / 2;
+    for (int i = 0; i < Hq; ++i)
+        for (int j = 0; j < Wq; ++j) {
+            double m = acc[(2 * i) * Wo + 2 * j];
+            double a = ab[(2 * i) * Wo + 2 * j];
+            for (int di = 0; di < 2; ++di)
+                for (int dj = 0; dj < 2; ++dj) {
+                    const double v = acc[(2 * i + di) * Wo + 2 * j + dj];
+                    const double t = ab[(2 * i + di) * Wo + 2 * j + dj];
+                    if (v > m) m = v;
+                    if (t > a) a = t;
+                }
+            out[i * Wq + j] = m;
+            absout[i * Wq + j] = a;
+        }
+}
+
+/*
+ * Fused sparse convolution over dense-stored sparse weights.
+ *   x      [N][C][H][W] fp32 (unpadded)
+ *   w      [K][C][R][S] fp32, mask same shape (nullable, see oracle_is_entry)
+ *   bias   [K] (nullable = zero bias)
+ *   pairs  nullable; if given, npairs (n, k) pairs, and out/absout hold one
+ *          plane per pair in that order; otherwise all N*K planes, n-major.
+ *   out, absout: double, plane size Ho*Wo, or (Ho/2)*(Wo/2) when pooling.
+ *   nthreads: OpenMP threads (<= 0: the runtime default).
+ * Returns 0, or -1 when the shapes give an empty output.
+ */
+int oracle_conv(const float *x, int N, int C, int H, int W, const float *w, const uint8_t *mask, int K, int R,
+                int S, const float *bias, int stride, int pad, int relu, int pool, const int32_t *pairs,
+                int npairs, double *out, double *absout, int nthreads) {
+    const int Ho = oracle_out_extent(H, R, stride, pad);
+    const int Wo = oracle_out_extent(W, S, stride, pad);
+    if (Ho < 1 || Wo < 1) return -1;
+    const int Hq = pool ? Ho / 2 : Ho, Wq = pool ? Wo / 2 : Wo;
+    const long long plane_out = (long long)Hq * Wq;
+    const long long nplanes = pairs ? npairs : (long long)N * K;
+#ifdef _OPENMP
+    if (nthreads <= 0) nthreads = omp_get_max_threads();
+#pragma omp parallel num_threads(nthreads)
+#endif
+    {
+        double *acc = (double *)malloc(sizeof(double) * Ho * Wo);
+        double *ab = (double *)malloc(sizeof(double) * Ho * Wo);
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+        for (long long p = 0; p < nplanes; ++p) {
+            const int n = pairs ? pairs[2 * p] : (int)(p / K);
+            const int k = pairs ? pairs[2 * p + 1] : (int)(p % K);
+            oracle_plane(x, C, H, W, w, mask, R, S, bias, stride, pad, relu, pool, n, k, acc, ab,
+                         out + p * plane_out, absout + p * plane_out);
+        }
+        free(acc);
+        free(ab);
+    }
+    return 0;
+}
+
+/* Number of threads the OpenMP runtime would use by default. */
+int oracle_max_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
