@@ -1,0 +1,191 @@
+"""Benchmark of the fused sparse convolution on one MI355X.
+
+One step = the whole hot path on one batch: zero-pad the NCHW input
+(spconv_pad_input), then the fused sparse conv + bias + ReLU (+ 2x2 max-pool)
+(spconv_forward). Inputs are seeded synthetic layers already resident in HBM.
+Prints one JSON line (rank 0) with the throughput in nonzero GFLOP/s, ms/layer,
+the fraction of the HBM roofline, a roofline record for the dominant kernel and
+the CPU oracle's rate on the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+from pathlib import Path
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, published
+VALU_FP32_FMA_TFLOPS = 78.6     # 256 CU x 64 lanes x 2 FLOP x 2.4 GHz (v_fma_f32; packed FP32 forms not used)
+FP32_VECTOR_PUBLISHED_TFLOPS = 157.3
+
+WORKLOADS = {
+    "resnet": "ResNet-style sparse conv: N=32, C=K=64, 56x56, 3x3, stride 1, pad 1, density 0.2, bias+ReLU, fp32",
+    "tiny": "tiny sparse conv: N=1, C=K=16, 16x16, 3x3, stride 1, pad 1, density 0.2, bias+ReLU, fp32",
+    "conv_pool": "sparse conv + pool: N=32, C=K=128, 28x28 -> 14x14, 3x3, density 0.1, bias+ReLU+2x2 max-pool, fp32",
+    "narrow_d0.05": "deep narrow: N=32, C=K=256, 14x14, 3x3, density 0.05 (Beta(2,5) row skew), bias+ReLU, fp32",
+    "narrow_d0.2": "deep narrow: N=32, C=K=256, 14x14, 3x3, density 0.2 (Beta(2,5) row skew), bias+ReLU, fp32",
+    "narrow_d0.5": "deep narrow: N=32, C=K=256, 14x14, 3x3, density 0.5 (Beta(2,5) row skew), bias+ReLU, fp32",
+}
+
+
+def algorithmic(layer, nnz):
+    """Nonzero FLOPs and algorithmic HBM bytes of one fused layer (pad excluded):
+    FLOPs = 2 * nnz * N * Ho * Wo; bytes = padded input read once + final output
+    written once + 8 B per nonzero (offset, value) + rowptr and bias."""
+    N, C, H, W, K, R, S = layer.shape
+    Hp, Wp = H + 2 * layer.pad, W + 2 * layer.pad
+    Ho = (Hp - R) // layer.stride + 1
+    Wo = (Wp - S) // layer.stride + 1
+    Hq, Wq = (Ho // 2, Wo // 2) if layer.pool else (Ho, Wo)
+    flops = 2.0 * nnz * N * Ho * Wo
+    fwd_bytes = 4.0 * N * C * Hp * Wp + 4.0 * N * K * Hq * Wq + 8.0 * nnz + 4.0 * (2 * K + 1)
+    pad_bytes = 4.0 * N * C * H * W + 4.0 * N * C * Hp * Wp
+    return flops, fwd_bytes, pad_bytes
+
+
+def cpu_baseline(layer, budget_s: float):
+    """Time the CPU oracle on a bounded sample of the same layer: whole output
+    planes (n, k), as many as fit the time budget (estimated from a first probe)."""
+    import numpy as np
+    import oracle
+
+    N, C, H, W, K, R, S = layer.shape
+    orc = oracle.get()
+    threads = orc.max_threads()
+    total = N * K
+    rng = np.random.default_rng(0)
+    order = rng.permutation(total)
+    probe = max(threads, 8)
+    pairs = [(int(p // K), int(p % K)) for p in order[:probe]]
+    t0 = time.perf_counter()
+    orc.conv(layer.x, layer.w, layer.mask, layer.bias, layer.stride, layer.pad, layer.relu, layer.pool, pairs=pairs)
+    dt = time.perf_counter() - t0
+    per_plane = dt / probe
+    count = int(min(total, max(probe, budget_s / max(per_plane, 1e-9))))
+    pairs = [(int(p // K), int(p % K)) for p in order[:count]]
+    t0 = time.perf_counter()
+    orc.conv(layer.x, layer.w, layer.mask, layer.bias, layer.stride, layer.pad, layer.relu, layer.pool, pairs=pairs)
+    dt = time.perf_counter() - t0
+    rowptr = np.concatenate([[0], np.cumsum((layer.mask.reshape(K, -1) != 0).sum(1))])
+    row_nnz = np.diff(rowptr)
+    Hp, Wp = H + 2 * layer.pad, W + 2 * layer.pad
+    Ho = (Hp - R) // layer.stride + 1
+    Wo = (Wp - S) // layer.stride + 1
+    flops = sum(2.0 * row_nnz[k] * Ho * Wo for _, k in pairs)
+    return {"value": flops / dt / 1e9, "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"{count} of {total} output planes (n, k) of the same layer, chosen at random; {dt:.1f} s",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="resnet", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2005_04091_amd import spconv, synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    layer = synth.make_layer(args.workload)
+    N, C, H, W, K, R, S = layer.shape
+    print(f"[bench] workload {args.workload}: {WORKLOADS[args.workload]}", file=sys.stderr, flush=True)
+    L = spconv.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, layer.stride, layer.pad, layer.relu,
+                               layer.pool, device=dev)
+    nnz = L.host_csr.nnz
+    x = torch.from_numpy(layer.x).to(dev)
+    xp = torch.empty((N, C, H + 2 * layer.pad, W + 2 * layer.pad), dtype=torch.float32, device=dev)
+    out = torch.empty((N, K, L.Ho, L.Wo), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    for _ in range(args.warmup):
+        L.run(x, xp=xp, out=out, stream=stream)
+    torch.cuda.synchronize()
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_all0 = torch.cuda.Event(enable_timing=True)
+    t_all1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_all0.record(stream)
+    for e0, e1, e2 in ev:
+        e0.record(stream)
+        L.pad_input(x, out=xp, stream=stream)
+        e1.record(stream)
+        L.forward_padded(xp, out=out, stream=stream)
+        e2.record(stream)
+    t_all1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_all0.elapsed_time(t_all1)
+    pad_ms = [a.elapsed_time(b) for a, b, _ in ev]
+    fwd_ms = [b.elapsed_time(c) for _, b, c in ev]
+    ms_per_step = total_ms / args.steps
+    fwd_avg = sum(fwd_ms) / len(fwd_ms)
+    fwd_med = statistics.median(fwd_ms)
+
+    flops, fwd_bytes, pad_bytes = algorithmic(layer, nnz)
+    value = flops / (ms_per_step * 1e-3) / 1e9
+    achieved_tflops = flops / (fwd_avg * 1e-3) / 1e12
+    rec = {
+        "metric": "ms/layer + nonzero GFLOP/s + % HBM roofline, fused sparse conv, 1 MI355X",
+        "value": round(value, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Bernoulli-masked weights U[-1,1), input U[0,1), bias U[-0.1,0.1))",
+        "config": {"workload": WORKLOADS[args.workload], "N": N, "C": C, "K": K, "H": H, "W": W, "R": R, "S": S,
+                   "stride": layer.stride, "pad": layer.pad, "pool": layer.pool, "nnz": nnz,
+                   "density": round(nnz / (K * C * R * S), 5)},
+        "ms_per_layer": round(fwd_avg, 5),
+        "ms_per_layer_median": round(fwd_med, 5),
+        "ms_pad": round(sum(pad_ms) / len(pad_ms), 5),
+        "nonzero_gflops_layer": round(flops / (fwd_avg * 1e-3) / 1e9, 2),
+        "hbm_roofline_frac": round(fwd_bytes / (fwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "roofline": {
+            "kernel": "spconv_fwd_kernel",
+            "bound": "alu",
+            "achieved": round(achieved_tflops, 3),
+            "peak": VALU_FP32_FMA_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved_tflops / VALU_FP32_FMA_TFLOPS, 4),
+            "traffic": None,
+            "algorithmic_bytes": int(fwd_bytes),
+            "flops": flops,
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        cb = cpu_baseline(layer, args.cpu_budget)
+        cb.pop("seconds", None)
+        cb["value"] = round(cb["value"], 3)
+        rec["cpu_baseline"] = cb
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

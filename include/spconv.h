@@ -1,0 +1,147 @@
+/*
+ * spconv.h - fused sparse direct convolution on MI355X (gfx950).
+ *
+ * C ABI of libspconv.so. The operation is the sparse direct convolution of the
+ * paper's "Optimizing Sparse Neural Networks" section (paragraph "Sparse
+ * Convolution with CSR"): the filter of shape (K, C, R, S) is viewed as a
+ * K x (C*R*S) matrix and its rows are compressed (CSR); for every output channel
+ * k and every nonzero (offset, coeff) of row k, each output pixel accumulates
+ * coeff times the padded input at the pixel's position plus the offset. The
+ * output is the dense convolution written in the paper's DSL section (read as a
+ * cross-correlation over the zero-padded input, no filter flip) followed, when
+ * requested, by the ReLU and 2x2 max-pool of its "Conv-Relu-Maxpool" block
+ * (section "Evaluation"), all fused into one kernel and one store.
+ *
+ * Layouts are NCHW, fp32, row-major. Hp = H + 2*pad, Wp = W + 2*pad,
+ * Ho = (Hp - R)/stride + 1, Wo = (Wp - S)/stride + 1 (floor); with the pool flag
+ * the stored output is Ho/2 x Wo/2 (floor: an odd last row/column is dropped).
+ *
+ * Every call returns an int status (SPCONV_OK or a negative code) and never
+ * throws. Argument checks happen on the host before any GPU work is queued.
+ * The caller owns every buffer; the library keeps no state, so calls on
+ * different streams may run concurrently.
+ */
+#ifndef SPCONV_H
+#define SPCONV_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define SPCONV_OK 0
+#define SPCONV_EINVAL (-1)    /* invalid argument; nothing was queued */
+#define SPCONV_ECAPACITY (-2) /* output arrays too small for the nonzeros (pack) */
+#define SPCONV_EHIP (-3)      /* a HIP call or kernel launch failed */
+
+/* Epilogue flags for spconv_forward. Any other bit is SPCONV_EINVAL. */
+#define SPCONV_RELU 1u       /* out = max(pre, 0) */
+#define SPCONV_MAXPOOL2X2 2u /* 2x2 window, stride 2, applied after the ReLU */
+
+/*
+ * CSR filter (paper, "Sparse Convolution with CSR": flatten (K, C, k, k) to
+ * (K, C*k*k), compress the rows). Besides the flattened column the entries carry
+ * the paper's input offset, lowered for a padded plane of Hp x Wp:
+ *   colidx[j] = c*R*S + r*S + s
+ *   offset[j] = c*Hp*Wp + r*Wp + s      (index inside one padded C x Hp x Wp image)
+ * Within a row, entries are in increasing colidx order. Pointers are host
+ * memory for spconv_pack_csr and device memory for spconv_forward; the struct
+ * itself is always a host object.
+ */
+typedef struct spconv_csr {
+    int32_t K, C, R, S; /* filter shape */
+    int32_t Hp, Wp;     /* padded plane the offsets were lowered for */
+    int64_t nnz;        /* number of entries, < 2^31 */
+    const int32_t *rowptr; /* [K+1]; rowptr[0] = 0, non-decreasing, rowptr[K] = nnz */
+    const int32_t *colidx; /* [nnz]; not read by spconv_forward (may be NULL there) */
+    const int32_t *offset; /* [nnz] */
+    const float *vals;     /* [nnz]; the filter values, bit-copied */
+} spconv_csr;
+
+/*
+ * spconv_pack_csr - host-side CSR packing of a dense-stored sparse filter.
+ *
+ * w      [K][C][R][S] fp32, host.
+ * mask   [K][C][R][S] bytes, host, nullable. With a mask, every position whose
+ *        byte is nonzero is an entry (an explicit 0.0 value is kept); without
+ *        one, every value that compares unequal to 0.0f is an entry (-0.0 is
+ *        dropped, NaN kept).
+ * Hp, Wp padded plane the offsets are lowered for; requires Hp >= R, Wp >= S.
+ * rowptr [K+1] int32, host, nullable only in the count phase.
+ * colidx, offset, vals  [capacity] host arrays. If all three are NULL the call
+ *        only counts: *nnz_out receives the number of entries (and rowptr is
+ *        filled when given).
+ * capacity  length of colidx/offset/vals; if the filter has more entries the
+ *        call returns SPCONV_ECAPACITY, sets *nnz_out to the count and writes
+ *        nothing else.
+ * nnz_out   host, required.
+ * Errors: SPCONV_EINVAL for NULL w/nnz_out, non-positive sizes, Hp < R,
+ * Wp < S, an offset or entry count that does not fit int32, or a partial set
+ * of output arrays.
+ */
+int spconv_pack_csr(const float *w, const uint8_t *mask, int K, int C, int R, int S, int Hp, int Wp,
+                    int32_t *rowptr, int32_t *colidx, int32_t *offset, float *vals, int64_t capacity,
+                    int64_t *nnz_out);
+
+/*
+ * spconv_pad_input - zero-padded copy of an NCHW tensor (device, asynchronous).
+ *
+ * The padded input is what the paper's CSR loop indexes with its offsets: it
+ * reads in[pixel + offset] with no bounds test, which needs the zero border.
+ *   out_padded[n][c][y+pad][x+pad] = in[n][c][y][x], border = +0.0.
+ * in          [N][C][H][W] fp32, device.
+ * out_padded  [N][C][H+2pad][W+2pad] fp32, device, must not overlap `in`.
+ * stream      HIP stream the copy is queued on (0 = the null stream).
+ * Errors: SPCONV_EINVAL (NULL pointer, N/C/H/W < 1, pad < 0, element count
+ * >= 2^40); SPCONV_EHIP when the launch fails.
+ */
+int spconv_pad_input(const float *in, int N, int C, int H, int W, int pad, float *out_padded, hipStream_t stream);
+
+/*
+ * spconv_forward - fused sparse convolution + bias + ReLU + 2x2 max-pool
+ * (device, asynchronous, one kernel, one store per output element).
+ *
+ *   pre[n,k,y,x] = bias[k] + sum_{j in row k} vals[j] *
+ *                  in_padded[n*C*Hp*Wp + (y*stride)*Wp + x*stride + offset[j]]
+ *   o   = (flags & SPCONV_RELU) ? max(pre, 0) : pre
+ *   out = (flags & SPCONV_MAXPOOL2X2) ? max over a,b in {0,1} of o[n,k,2i+a,2j+b] : o
+ *
+ * in_padded  [N][C][Hp][Wp] fp32, device: the zero-bordered input (as written by
+ *            spconv_pad_input).
+ * csr        host struct whose arrays are in device memory; csr->K/C/R/S must
+ *            equal K/C/R/S and csr->Hp/Wp must equal H+2pad / W+2pad. The array
+ *            contents must be a valid CSR as produced by spconv_pack_csr for
+ *            these Hp/Wp; they are not re-validated on the device.
+ * bias       [K] fp32, device, nullable (zero bias).
+ * out        [N][K][Ho][Wo] fp32 (or [N][K][Ho/2][Wo/2] with the pool flag),
+ *            device, must not overlap the inputs. Every element is written.
+ * stream     HIP stream the kernel is queued on (0 = the null stream).
+ * Summation order inside one output is unspecified (fp32 arithmetic; results
+ * are reproducible run to run for a given device and shape).
+ * Errors: SPCONV_EINVAL (NULL pointer, sizes < 1, stride < 1, pad < 0, shape
+ * mismatch with csr, nnz outside [0, 2^31), unknown flag bits, empty output,
+ * Ho or Wo < 2 with the pool flag, C*Hp*Wp >= 2^31); SPCONV_EHIP when the
+ * launch fails.
+ */
+int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S,
+                   int stride, int pad, const float *bias, uint32_t flags, float *out, hipStream_t stream);
+
+/*
+ * spconv_output_shape - stored output plane size for the given layer.
+ * Writes *Ho, *Wo (pooled sizes when flags has SPCONV_MAXPOOL2X2).
+ * Errors: SPCONV_EINVAL for NULL outputs, H/W/R/S/stride < 1, pad < 0, unknown
+ * flags, or an empty (pooled) output.
+ */
+int spconv_output_shape(int H, int W, int R, int S, int stride, int pad, uint32_t flags, int *Ho, int *Wo);
+
+/* spconv_strerror - static, human-readable text for a status code. */
+const char *spconv_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPCONV_H */

@@ -1,0 +1,217 @@
+"""Python binding of libspconv.so (C ABI declared in include/spconv.h).
+
+Argument marshalling only: host arrays are numpy, device buffers are torch CUDA
+(HIP) tensors, streams are torch streams. Every computation happens in the
+library. Importing this module loads the library and raises ImportError if it
+has not been built (``python -m paper_2005_04091_amd.build``).
+"""
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from pathlib import Path
+
+import numpy as np
+
+LIB_PATH = Path(__file__).resolve().parent / "libspconv.so"
+if not LIB_PATH.exists():
+    raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2005_04091_amd.build` first")
+
+_lib = ctypes.CDLL(str(LIB_PATH))
+
+SPCONV_OK = 0
+SPCONV_EINVAL = -1
+SPCONV_ECAPACITY = -2
+SPCONV_EHIP = -3
+SPCONV_RELU = 1
+SPCONV_MAXPOOL2X2 = 2
+
+EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_output_shape", "spconv_strerror")
+
+
+class spconv_csr(ctypes.Structure):
+    """Mirror of ``struct spconv_csr``."""
+    _fields_ = [("K", ctypes.c_int32), ("C", ctypes.c_int32), ("R", ctypes.c_int32), ("S", ctypes.c_int32),
+                ("Hp", ctypes.c_int32), ("Wp", ctypes.c_int32), ("nnz", ctypes.c_int64),
+                ("rowptr", ctypes.c_void_p), ("colidx", ctypes.c_void_p), ("offset", ctypes.c_void_p),
+                ("vals", ctypes.c_void_p)]
+
+
+_c_int = ctypes.c_int
+_vp = ctypes.c_void_p
+_lib.spconv_pack_csr.restype = _c_int
+_lib.spconv_pack_csr.argtypes = [_vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp, _vp,
+                                 ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
+_lib.spconv_pad_input.restype = _c_int
+_lib.spconv_pad_input.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp]
+_lib.spconv_forward.restype = _c_int
+_lib.spconv_forward.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int,
+                                _c_int, _c_int, _c_int, _vp, ctypes.c_uint32, _vp, _vp]
+_lib.spconv_output_shape.restype = _c_int
+_lib.spconv_output_shape.argtypes = [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_uint32,
+                                     ctypes.POINTER(_c_int), ctypes.POINTER(_c_int)]
+_lib.spconv_strerror.restype = ctypes.c_char_p
+_lib.spconv_strerror.argtypes = [_c_int]
+
+
+class SpconvError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {spconv_strerror(code)} ({code})")
+
+
+def _check(code: int, what: str):
+    if code != SPCONV_OK:
+        raise SpconvError(code, what)
+
+
+def spconv_strerror(code: int) -> str:
+    return _lib.spconv_strerror(int(code)).decode()
+
+
+def spconv_output_shape(H, W, R, S, stride, pad, flags):
+    ho, wo = _c_int(), _c_int()
+    _check(_lib.spconv_output_shape(H, W, R, S, stride, pad, flags, ctypes.byref(ho), ctypes.byref(wo)),
+           "spconv_output_shape")
+    return ho.value, wo.value
+
+
+@dataclass
+class HostCSR:
+    """CSR filter in host memory, as written by ``spconv_pack_csr``."""
+    K: int
+    C: int
+    R: int
+    S: int
+    Hp: int
+    Wp: int
+    rowptr: np.ndarray
+    colidx: np.ndarray
+    offset: np.ndarray
+    vals: np.ndarray
+
+    @property
+    def nnz(self) -> int:
+        return int(self.colidx.size)
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def spconv_pack_csr(w: np.ndarray, mask: np.ndarray | None, Hp: int, Wp: int) -> HostCSR:
+    """Two-phase call of ``spconv_pack_csr`` (count, then fill) on host arrays."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    if w.ndim != 4:
+        raise ValueError("w must be [K, C, R, S]")
+    K, C, R, S = (int(v) for v in w.shape)
+    m = None
+    if mask is not None:
+        m = np.ascontiguousarray(mask, dtype=np.uint8)
+        if m.shape != w.shape:
+            raise ValueError("mask must have the weight's shape")
+    nnz = ctypes.c_int64()
+    rowptr = np.zeros(K + 1, np.int32)
+    _check(_lib.spconv_pack_csr(_np_ptr(w), _np_ptr(m), K, C, R, S, Hp, Wp, _np_ptr(rowptr), None, None, None, 0,
+                                ctypes.byref(nnz)), "spconv_pack_csr (count)")
+    n = nnz.value
+    colidx = np.zeros(max(n, 1), np.int32)
+    offset = np.zeros(max(n, 1), np.int32)
+    vals = np.zeros(max(n, 1), np.float32)
+    _check(_lib.spconv_pack_csr(_np_ptr(w), _np_ptr(m), K, C, R, S, Hp, Wp, _np_ptr(rowptr), _np_ptr(colidx),
+                                _np_ptr(offset), _np_ptr(vals), n, ctypes.byref(nnz)), "spconv_pack_csr")
+    return HostCSR(K, C, R, S, Hp, Wp, rowptr, colidx[:n], offset[:n], vals[:n])
+
+
+class DeviceCSR:
+    """A HostCSR copied to device memory (torch tensors) plus its C struct."""
+
+    def __init__(self, host: HostCSR, device="cuda"):
+        import torch
+        self.host = host
+        self.rowptr = torch.from_numpy(host.rowptr).to(device)
+        # Keep at least one element so the device pointers are valid even when nnz == 0.
+        self.colidx = torch.from_numpy(np.concatenate([host.colidx, np.zeros(1, np.int32)])).to(device)
+        self.offset = torch.from_numpy(np.concatenate([host.offset, np.zeros(1, np.int32)])).to(device)
+        self.vals = torch.from_numpy(np.concatenate([host.vals, np.zeros(1, np.float32)])).to(device)
+        self.struct = spconv_csr(host.K, host.C, host.R, host.S, host.Hp, host.Wp, host.nnz,
+                                 self.rowptr.data_ptr(), self.colidx.data_ptr(), self.offset.data_ptr(),
+                                 self.vals.data_ptr())
+
+
+def _dev_ptr(t, name):
+    import torch
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != torch.float32 or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous float32 tensor")
+    return t.data_ptr()
+
+
+def _stream_handle(stream, device):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return s.cuda_stream
+
+
+def spconv_pad_input(x, pad: int, out=None, stream=None):
+    """Zero-padded copy of NCHW ``x`` (device), queued on ``stream``."""
+    import torch
+    if x.dim() != 4:
+        raise ValueError("x must be NCHW")
+    N, C, H, W = (int(v) for v in x.shape)
+    if out is None:
+        out = torch.empty((N, C, H + 2 * pad, W + 2 * pad), dtype=torch.float32, device=x.device)
+    _check(_lib.spconv_pad_input(_dev_ptr(x, "x"), N, C, H, W, pad, _dev_ptr(out, "out"),
+                                 _stream_handle(stream, x.device)), "spconv_pad_input")
+    return out
+
+
+def spconv_forward(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int,
+                   pad: int, bias=None, flags: int = SPCONV_RELU, out=None, stream=None):
+    """Fused sparse conv + bias + ReLU (+ 2x2 max-pool) on the padded input ``xp``."""
+    import torch
+    Ho, Wo = spconv_output_shape(H, W, R, S, stride, pad, flags)
+    if out is None:
+        out = torch.empty((N, K, Ho, Wo), dtype=torch.float32, device=xp.device)
+    _check(_lib.spconv_forward(_dev_ptr(xp, "xp"), N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad,
+                               _dev_ptr(bias, "bias"), flags, _dev_ptr(out, "out"),
+                               _stream_handle(stream, xp.device)), "spconv_forward")
+    return out
+
+
+def flags_of(relu: bool, pool: bool) -> int:
+    return (SPCONV_RELU if relu else 0) | (SPCONV_MAXPOOL2X2 if pool else 0)
+
+
+class SparseConvLayer:
+    """One layer's device state: the packed CSR, bias and shape, ready to run.
+
+    ``run(x)`` queues pad + fused forward on the current stream and returns the
+    output tensor.
+    """
+
+    def __init__(self, w: np.ndarray, mask: np.ndarray | None, bias: np.ndarray | None, H: int, W: int,
+                 stride: int = 1, pad: int = 1, relu: bool = True, pool: bool = False, device="cuda"):
+        import torch
+        self.K, self.C, self.R, self.S = (int(v) for v in w.shape)
+        self.H, self.W, self.stride, self.pad = H, W, stride, pad
+        self.flags = flags_of(relu, pool)
+        self.host_csr = spconv_pack_csr(w, mask, H + 2 * pad, W + 2 * pad)
+        self.csr = DeviceCSR(self.host_csr, device)
+        self.bias = None if bias is None else torch.from_numpy(np.ascontiguousarray(bias, np.float32)).to(device)
+        self.Ho, self.Wo = spconv_output_shape(H, W, self.R, self.S, stride, pad, self.flags)
+
+    def pad_input(self, x, out=None, stream=None):
+        return spconv_pad_input(x, self.pad, out=out, stream=stream)
+
+    def forward_padded(self, xp, out=None, stream=None):
+        N = int(xp.shape[0])
+        return spconv_forward(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
+                              self.pad, self.bias, self.flags, out=out, stream=stream)
+
+    def run(self, x, xp=None, out=None, stream=None):
+        xp = self.pad_input(x, out=xp, stream=stream)
+        return self.forward_padded(xp, out=out, stream=stream)

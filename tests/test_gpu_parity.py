@@ -1,0 +1,269 @@
+"""GPU parity: the HIP path against the CPU oracle, element by element.
+
+Acceptance per output element: |gpu - oracle| <= 1e-5 * A + 1e-6, where A is the
+oracle's sum of |w * x| over the terms of that output (its max over the window for
+pooled outputs). Index work (padding) is compared bit for bit. Every case prints
+its name and shape before touching the GPU.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2005_04091_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+REL_TOL = 1e-5
+ABS_TOL = 1e-6
+
+
+@pytest.fixture(scope="module")
+def sp():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2005_04091_amd import spconv
+    return spconv
+
+
+def say(*a):
+    print("[case]", *a, flush=True)
+
+
+def check_close(gpu, ref, ab, what=""):
+    gpu = np.asarray(gpu, np.float64)
+    assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
+    assert np.all(np.isfinite(gpu)), f"{what}: non-finite output"
+    err = np.abs(gpu - ref)
+    tol = REL_TOL * ab + ABS_TOL
+    bad = err > tol
+    if bad.any():
+        i = np.unravel_index(np.argmax(err - tol), err.shape)
+        raise AssertionError(f"{what}: {int(bad.sum())} of {bad.size} outputs out of tolerance; worst at {i}: "
+                             f"gpu={gpu[i]!r} oracle={ref[i]!r} A={ab[i]!r}")
+
+
+def run_layer(sp, layer, stream=None):
+    import torch
+    N, C, H, W, K, R, S = layer.shape
+    L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, layer.stride, layer.pad, layer.relu, layer.pool)
+    x = torch.from_numpy(layer.x).cuda()
+    out = L.run(x, stream=stream)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def oracle_layer(layer, pairs=None):
+    return oracle.conv(layer.x, layer.w, layer.mask, layer.bias, layer.stride, layer.pad, layer.relu, layer.pool,
+                       pairs=pairs)
+
+
+# ---------------------------------------------------------------------------
+# Padded input: bit exact against numpy.pad
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape,pad", [((1, 1, 1, 1), 0), ((1, 1, 1, 1), 3), ((2, 3, 5, 7), 1), ((3, 2, 17, 9), 2),
+                                       ((2, 4, 56, 56), 1), ((1, 3, 33, 65), 0), ((4, 5, 13, 300), 4)])
+def test_pad_bit_exact(sp, shape, pad):
+    import torch
+    say("pad", shape, pad)
+    rng = np.random.default_rng(sum(shape) + pad)
+    x = rng.uniform(-1, 1, shape).astype(np.float32)
+    x.reshape(-1)[::7] = -0.0
+    xp = sp.spconv_pad_input(torch.from_numpy(x).cuda(), pad)
+    torch.cuda.synchronize()
+    ref = oracle.pad(x, pad)
+    assert np.array_equal(xp.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# Forward: small shapes spanning tiles, ragged tails and the degenerate cases
+# ---------------------------------------------------------------------------
+
+SWEEP = [
+    # N, C, K, H, W, R, S, stride, pad, density, relu, pool, bias, skew
+    (1, 16, 16, 16, 16, 3, 3, 1, 1, 0.2, True, False, True, False),
+    (2, 3, 5, 7, 9, 3, 3, 1, 1, 0.5, True, False, True, False),      # odd, H != W, K ragged
+    (3, 4, 6, 11, 13, 3, 3, 1, 0, 0.3, False, False, True, False),   # pad 0, N ragged vs images per group
+    (2, 5, 7, 9, 8, 3, 3, 2, 1, 0.4, True, False, True, False),      # stride 2
+    (2, 5, 3, 10, 12, 3, 3, 2, 1, 0.4, True, True, True, False),     # stride 2 + pool
+    (1, 6, 9, 12, 10, 5, 5, 1, 2, 0.3, True, False, False, False),   # 5x5, no bias
+    (2, 4, 8, 9, 15, 3, 1, 1, 1, 0.5, True, False, True, False),     # 3x1
+    (2, 4, 8, 9, 15, 1, 3, 1, 1, 0.5, True, False, True, False),     # 1x3 (pad makes Ho > H)
+    (2, 8, 12, 14, 14, 1, 1, 1, 0, 0.5, True, False, True, False),   # 1x1
+    (2, 3, 4, 8, 8, 2, 2, 1, 0, 0.6, True, True, True, False),       # 2x2, pool
+    (2, 8, 10, 13, 11, 3, 3, 1, 1, 0.3, True, True, True, False),    # pool with odd Ho/Wo (floor)
+    (1, 2, 3, 6, 6, 3, 3, 1, 1, 0.0, True, False, True, False),      # density 0: act(bias)
+    (2, 3, 5, 6, 7, 3, 3, 1, 1, 1.0, False, False, True, False),     # density 1, no ReLU
+    (2, 200, 9, 10, 10, 3, 3, 1, 1, 0.1, True, False, True, False),  # C spans several LDS chunks
+    (2, 64, 33, 20, 20, 3, 3, 1, 1, 0.2, True, False, True, True),   # skewed rows, K ragged vs 8
+    (1, 8, 16, 60, 64, 3, 3, 1, 1, 0.2, True, False, True, False),   # several spatial tiles
+    (2, 8, 16, 61, 70, 3, 3, 1, 1, 0.2, True, True, True, False),    # several tiles + pool, odd Ho
+    (1, 4, 4, 5, 300, 3, 3, 1, 1, 0.3, True, False, True, False),    # wide rows (tile < one row pair)
+    (5, 16, 20, 14, 14, 3, 3, 1, 1, 0.05, True, False, True, False), # small planes, several images per group
+    (1, 1, 1, 1, 1, 1, 1, 1, 0, 1.0, False, False, True, False),     # 1x1x1x1
+    (2, 3, 4, 2, 2, 3, 3, 1, 1, 0.7, True, True, True, False),       # tiny pooled output (1x1)
+]
+
+
+@pytest.mark.parametrize("case", SWEEP, ids=[f"sweep{i}" for i in range(len(SWEEP))])
+def test_forward_sweep(sp, case):
+    N, C, K, H, W, R, S, stride, pad, d, relu, pool, bias, skew = case
+    layer = synth.random_layer(1000 + hash(case) % 1000, N, C, K, H, W, R, S, stride, pad, d, relu, pool, bias, skew)
+    say("sweep", case)
+    gpu = run_layer(sp, layer)
+    ref, ab = oracle_layer(layer)
+    check_close(gpu, ref, ab, f"sweep {case}")
+
+
+def test_single_row_holds_every_nonzero(sp):
+    """Maximal skew: one output channel has every tap, the others none."""
+    layer = synth.random_layer(77, 2, 32, 12, 18, 18, 3, 3, 1, 1, 1.0, True, False, True)
+    layer.mask[:] = 0
+    layer.mask[5] = 1
+    layer.w = np.where(layer.mask != 0, np.random.default_rng(1).uniform(-1, 1, layer.w.shape), 0).astype(np.float32)
+    say("single-row skew")
+    gpu = run_layer(sp, layer)
+    ref, ab = oracle_layer(layer)
+    check_close(gpu, ref, ab, "single row")
+
+
+def test_identity_filter_bitwise(sp):
+    """One 1.0 per row at (c = k, centre tap): output == input bit for bit, and
+    with pooling the 2x2 block max of the input."""
+    rng = np.random.default_rng(3)
+    N, C, H, W = 3, 24, 30, 27
+    x = rng.random((N, C, H, W), dtype=np.float32)
+    w = np.zeros((C, C, 3, 3), np.float32)
+    for k in range(C):
+        w[k, k, 1, 1] = 1.0
+    for pool in (False, True):
+        layer = synth.Layer("identity", x, w, (w != 0).astype(np.uint8), None, 1, 1, True, pool)
+        say("identity", pool)
+        gpu = run_layer(sp, layer)
+        ref = x if not pool else x[:, :, :H // 2 * 2, :W // 2 * 2].reshape(N, C, H // 2, 2, W // 2, 2).max(axis=(3, 5))
+        assert np.array_equal(gpu.view(np.uint32), ref.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# The named layers at full size, in the launch configuration the benchmark uses
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["tiny", "resnet", "conv_pool", "narrow_d0.05", "narrow_d0.2", "narrow_d0.5"])
+def test_named_layer_full(sp, name):
+    layer = synth.make_layer(name)
+    say("layer", name, layer.shape)
+    gpu = run_layer(sp, layer)
+    ref, ab = oracle_layer(layer)
+    check_close(gpu, ref, ab, name)
+
+
+def _sample_pairs(N, K, count, seed):
+    rng = np.random.default_rng(seed)
+    return [(int(rng.integers(N)), int(rng.integers(K))) for _ in range(count)]
+
+
+@pytest.mark.parametrize("which", [1, 2])
+def test_vgg_layers_full_size_sampled(sp, which):
+    """Each VGG-block layer at 32 x 64 x 224 x 224, checked on sampled output
+    planes the oracle computes one by one."""
+    _, l1, l2 = synth.make_vgg_block()
+    layer = l1 if which == 1 else l2
+    N, C, H, W, K, R, S = layer.shape
+    say("vgg layer", which, layer.shape)
+    gpu = run_layer(sp, layer)
+    pairs = _sample_pairs(N, K, 12, which)
+    ref, ab = oracle_layer(layer, pairs)
+    got = np.stack([gpu[n, k] for n, k in pairs])
+    check_close(got, ref, ab, f"vgg layer {which}")
+
+
+def _chain_check(sp, x, l1, l2, images, pairs_per_image, seed):
+    """Chained layers on the GPU (layer 2 reads layer 1's GPU output) against the
+    oracle chain (layer 2 applied to layer 1's oracle output rounded to fp32).
+    The bound adds, to layer 2's own tolerance, the propagated layer-1 error
+    sum |w2| * (1e-5*A1 + 1e-6 + |y1| * 2^-24), evaluated by the oracle itself
+    (ReLU and max-pool are 1-Lipschitz)."""
+    import torch
+    N, C, H, W, K, R, S = l1.shape
+    L1 = sp.SparseConvLayer(l1.w, l1.mask, l1.bias, H, W, 1, 1, l1.relu, l1.pool)
+    L2 = sp.SparseConvLayer(l2.w, l2.mask, l2.bias, H, W, 1, 1, l2.relu, l2.pool)
+    y1 = L1.run(torch.from_numpy(x).cuda())
+    y2 = L2.run(y1)
+    torch.cuda.synchronize()
+    y2 = y2.cpu().numpy()
+    rng = np.random.default_rng(seed)
+    for n in images:
+        xo = x[n:n + 1]
+        r1, a1 = oracle.conv(xo, l1.w, l1.mask, l1.bias, 1, 1, l1.relu, l1.pool)
+        x2 = r1.astype(np.float32)
+        ks = sorted(set(int(k) for k in rng.integers(0, K, pairs_per_image)))
+        pairs = [(0, k) for k in ks]
+        r2, a2 = oracle.conv(x2, l2.w, l2.mask, l2.bias, 1, 1, l2.relu, l2.pool, pairs=pairs)
+        delta = (REL_TOL * a1 + ABS_TOL + np.abs(r1) * 2.0 ** -24) * (1 + 1e-6)
+        prop, _ = oracle.conv(delta.astype(np.float32), np.abs(l2.w), l2.mask, None, 1, 1, False, l2.pool,
+                              pairs=pairs)
+        got = np.stack([y2[n, k] for k in ks]).astype(np.float64)
+        err = np.abs(got - r2)
+        tol = REL_TOL * a2 + ABS_TOL + prop
+        assert np.all(err <= tol), f"chain image {n}: {(err > tol).sum()} outputs out of bound"
+
+
+def test_chain_small(sp):
+    """Two chained layers at a size the oracle covers whole (VGG-block shape, scaled)."""
+    rng = np.random.default_rng(9)
+    N, C, K, H, W = 2, 8, 8, 32, 32
+    x = np.zeros((N, C, H, W), np.float32)
+    x[:, :3] = rng.random((N, 3, H, W), dtype=np.float32)
+    l1 = synth.random_layer(91, N, C, K, H, W, density=0.3, relu=True, pool=False)
+    l2 = synth.random_layer(92, N, K, K, H, W, density=0.3, relu=True, pool=True)
+    say("chain small")
+    _chain_check(sp, x, l1, l2, images=range(N), pairs_per_image=K, seed=5)
+
+
+def test_vgg_block_chain_full_size(sp):
+    """The VGG-style block as the benchmark runs it (32 images, chained), with
+    two images checked against the oracle chain."""
+    x, l1, l2 = synth.make_vgg_block()
+    say("vgg chain", x.shape)
+    _chain_check(sp, x, l1, l2, images=[0, 31], pairs_per_image=6, seed=6)
+
+
+# ---------------------------------------------------------------------------
+# Robustness
+# ---------------------------------------------------------------------------
+
+def test_guard_bands_and_full_coverage(sp):
+    """Output written exactly once per element: a NaN-filled buffer with guard
+    bands on both sides keeps its guards and has no NaN left inside."""
+    import torch
+    for pool in (False, True):
+        layer = synth.random_layer(55, 3, 12, 10, 19, 23, density=0.3, pool=pool)
+        N, C, H, W, K, R, S = layer.shape
+        L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, 1, 1, True, pool)
+        n_out = N * K * L.Ho * L.Wo
+        guard = 4096
+        buf = torch.full((n_out + 2 * guard,), float("nan"), dtype=torch.float32, device="cuda")
+        buf[:guard] = 7.0
+        buf[-guard:] = -7.0
+        out = buf[guard:guard + n_out].view(N, K, L.Ho, L.Wo)
+        say("guard", pool)
+        L.run(torch.from_numpy(layer.x).cuda(), out=out)
+        torch.cuda.synchronize()
+        b = buf.cpu().numpy()
+        assert np.all(b[:guard] == 7.0) and np.all(b[-guard:] == -7.0)
+        assert not np.isnan(b[guard:guard + n_out]).any()
+
+
+def test_deterministic_and_stream_ordered(sp):
+    """Repeated runs are bit-identical, also on a non-default stream."""
+    import torch
+    layer = synth.make_layer("tiny")
+    say("determinism")
+    a = run_layer(sp, layer)
+    b = run_layer(sp, layer)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        c = run_layer(sp, layer, stream=s)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    assert np.array_equal(a.view(np.uint32), c.view(np.uint32))
