@@ -1,26 +1,30 @@
 // Fused sparse direct convolution for MI355X (gfx950): padded-input kernel,
-// sparse gather-accumulate kernel with fused bias / ReLU / 2x2 max-pool, and
+// sparse gather-accumulate kernels with fused bias / ReLU / 2x2 max-pool, and
 // the C-ABI entry points that validate, plan the tiling and launch them.
 //
 // The method is the CSR direct convolution of the paper's "Sparse Convolution
 // with CSR" paragraph: for output channel k and each nonzero (offset, coeff) of
 // CSR row k, every output pixel p accumulates coeff * in_padded[p + offset].
-// With stride 1 and the padded row pitch Wp as the pixel pitch, pixel
-// (y, x) sits at p = y*Wp + x ("virtual" columns x >= Wo are computed and never
-// stored), so one nonzero moves a whole contiguous pixel range by one offset.
+// With stride 1 and the padded row pitch Wp as the pixel pitch, pixel (y, x)
+// sits at p = y*Wp + x ("virtual" columns x >= Wo are computed and never
+// stored), so one nonzero shifts a whole contiguous pixel range by one offset.
 //
-// Mapping to CDNA4:
-//  * a workgroup (4 wave64s) owns (image group, output-channel tile of KT rows,
-//    spatial tile of TH output rows at full width);
-//  * the padded input rows of the tile are staged in LDS one channel chunk at a
-//    time; the CSR rows are walked in order, the nonzeros of each row arriving
-//    through scalar loads, so every lane sees the same (offset, coeff);
-//  * lane l of a wave owns pixels q0 + l + 64*j (j < P): each LDS read of a wave
-//    touches 64 consecutive floats (no bank conflicts) and each global store of
-//    the epilogue is coalesced;
-//  * accumulators for all KT rows stay in VGPRs across the channel chunks; the
-//    epilogue adds the bias, applies ReLU and, for the pooled variant, reduces
-//    the 2x2 windows through an LDS staging tile before the single store.
+// Stride-1 kernel (the hot path), mapped to CDNA4:
+//  * a workgroup (4 wave64s) owns (group of IPW images, spatial tile of TH
+//    output rows at full width, tile of 4*RPW output channels); each wave owns
+//    RPW of those channels and every pixel of the tile;
+//  * the padded input rows of the tile are copied to LDS one channel chunk at
+//    a time with asynchronous global->LDS loads into two buffers, so the copy of
+//    chunk c+1 overlaps the arithmetic on chunk c;
+//  * each wave walks its CSR rows in order; the (offset, coeff) stream arrives
+//    through scalar loads, so all lanes see the same nonzero; the tap's LDS
+//    address is decoded from the offset on the scalar unit;
+//  * lane l owns pixels l + 64*j (j < PI) of each image, so each LDS read of a
+//    wave covers 64 consecutive floats (no bank conflicts) and the epilogue's
+//    global stores are coalesced;
+//  * accumulators stay in VGPRs across the chunks; the epilogue adds the bias,
+//    applies ReLU and, for the pooled variant, reduces 2x2 windows through an
+//    LDS staging tile before the single store.
 // MFMA is not used: at the densities this path serves, the work is a
 // gather-accumulate, not a dense contraction.
 #include <hip/hip_runtime.h>
@@ -37,7 +41,14 @@ constexpr int kWave = 64;
 constexpr int kWaves = 4;
 constexpr int kThreads = kWave * kWaves;
 constexpr int kXcds = 8;                  // MI355X: 8 XCDs, workgroups dispatched round-robin
-constexpr int kLdsBudgetFloats = 16384;   // 64 KiB of LDS per workgroup (two workgroups per CU)
+constexpr int kLdsBudgetFloats = 20480;   // generic kernel: 80 KiB of LDS per workgroup (two per CU)
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void global_void_t;
+
+__device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shift) {
+    return (uint32_t)(((uint64_t)x * (uint64_t)magic) >> shift);
+}
 
 // ---------------------------------------------------------------------------
 // Padded input (spconv_pad_input)
@@ -57,10 +68,6 @@ struct PadArgs {
     uint32_t wp_magic;    // x / Wp == (x * wp_magic) >> wp_shift for 0 <= x < 2^31
     int wp_shift;
 };
-
-__device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shift) {
-    return (uint32_t)(((uint64_t)x * (uint64_t)magic) >> shift);
-}
 
 __global__ __launch_bounds__(kThreads) void pad_nchw_kernel(PadArgs a) {
     const uint32_t plane_id = blockIdx.x / (uint32_t)a.blocks_per_plane;
@@ -85,26 +92,28 @@ __global__ __launch_bounds__(kThreads) void pad_nchw_kernel(PadArgs a) {
 // Sparse convolution (spconv_forward)
 // ---------------------------------------------------------------------------
 
+// Sizes and tiling of one launch. The buffers travel as separate __restrict__
+// kernel arguments: that is what lets the compiler fetch the CSR stream with
+// scalar loads (it must know no store or asynchronous LDS copy in the kernel
+// can modify them).
 struct FwdArgs {
-    const float *xp;        // [N][C][Hp][Wp]
-    const int32_t *rowptr;  // [K+1]
-    const int32_t *offset;  // [nnz]
-    const float *vals;      // [nnz]
-    const float *bias;      // [K] or null
-    float *out;
     int N, C, K, Hp, Wp, Ho, Wo, Hq, Wq, stride;
+    int nnz;
     int relu;
     // tiling
     int TH;            // output rows per spatial tile
     int ntiles_y;      // spatial tiles per image
     int ipw;           // images per workgroup
-    int wpi;           // waves per image
-    int nktiles;       // ceil(K / KT)
+    int wpi;           // waves per image (generic kernel)
+    int nktiles;       // ceil(K / rows per workgroup)
     int Cc;            // channels per LDS chunk
     int nchunks;
     int rows_in;       // padded input rows staged per tile
     int PL;            // LDS floats per staged channel (rows_in * Wp)
     int img_lds;       // LDS floats per image block (Cc * PL)
+    int PLp;           // LDS pitch of one staged channel (stride-1 kernel: PL rounded up to 256)
+    int buf_floats;    // LDS floats per chunk buffer (stride-1 kernel: two buffers)
+    size_t total_floats;  // N*C*Hp*Wp, the extent of the padded input
     int wv;            // pixel pitch of the virtual tile: Wp (stride 1) or Wo
     int total_wgs;
     uint32_t magic;    // c = offset / (Hp*Wp) == (offset * magic) >> shift
@@ -112,17 +121,314 @@ struct FwdArgs {
     int plane_delta;   // Hp*Wp - PL
 };
 
-// Workgroup id -> linear work index such that consecutive work items (the KT
-// tiles of one image tile, which read the same staged input) land on the same
-// XCD and therefore share its L2.
+// Workgroup id -> linear work index such that consecutive work items (the
+// channel tiles of one image tile, which read the same input rows) land on the
+// same XCD and therefore share its L2.
 __device__ __forceinline__ int xcd_linear_id(int b, int G) {
     const int xcd = b % kXcds, i = b / kXcds;
     const int per = G / kXcds, rem = G % kXcds;
     return (xcd < rem) ? xcd * (per + 1) + i : rem * (per + 1) + (xcd - rem) * per + i;
 }
 
-template <int P, int KT, bool S1, bool POOL>
-__global__ __launch_bounds__(kThreads) void spconv_fwd_kernel(FwdArgs a) {
+// Queue asynchronous global->LDS copies of one channel chunk: for each image of
+// the group and each channel of the chunk, seg_len consecutive floats (the
+// tile's padded input rows) land at buf + im*img_lds + cl*PL. Each wave copies
+// blocks of 64 floats, one per lane.
+__device__ __forceinline__ void stage_chunk(const FwdArgs &a, const float *__restrict__ xp, float *buf, int ch, int ig,
+                                            int in_row0, int seg_len, int wave, int lane) {
+    const int c0 = ch * a.Cc;
+    const int cn = min(a.Cc, a.C - c0);
+    const int nblk = (seg_len + kWave - 1) / kWave;
+    for (int im = 0; im < a.ipw; ++im) {
+        const int nn = ig * a.ipw + im;
+        if (nn >= a.N) break;
+        for (int cl = 0; cl < cn; ++cl) {
+            const float *src = xp + ((size_t)(nn * a.C + c0 + cl) * a.Hp + in_row0) * a.Wp;
+            float *dst = buf + im * a.img_lds + cl * a.PL;
+            for (int b = wave; b < nblk; b += kWaves) {
+                const int e = b * kWave + lane;
+                if (e < seg_len)
+                    __builtin_amdgcn_global_load_lds((global_void_t *)(src + e), (lds_void_t *)(dst + b * kWave), 4, 0,
+                                                     0);
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void wait_async_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// ---- Stride-1 kernel ------------------------------------------------------
+
+constexpr int kS1Waves = 8;
+constexpr int kS1Threads = kS1Waves * kWave;
+constexpr int kS1LdsFloats = 40960;  // 160 KiB: one workgroup per CU, two chunk buffers
+constexpr int kStageBlock = 256;     // floats per 16-byte-per-lane LDS DMA instruction
+
+// Queue the asynchronous copy of one channel chunk: for each image of the group
+// and each channel of the chunk, PLp floats starting at the tile's first padded
+// row land at buf + im*img_lds + cl*PLp. Every lane moves 16 bytes per
+// instruction (buffer_load_dwordx4 ... lds). Copies may run past the tile's rows
+// into the channel's LDS padding; the buffer range stops them at the end of the
+// input tensor (such lanes read 0).
+__device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__restrict__ xp, float *buf, int ch,
+                                               int ig, int in_row0, int wave, int lane) {
+    const int c0 = ch * a.Cc;
+    const int cn = min(a.Cc, a.C - c0);
+    const int nblk = a.PLp / kStageBlock;
+    const int plane = a.Hp * a.Wp;
+    for (int im = 0; im < a.ipw; ++im) {
+        const int nn = ig * a.ipw + im;
+        if (nn >= a.N) break;
+        const size_t first = ((size_t)(nn * a.C + c0) * a.Hp + in_row0) * a.Wp;
+        const size_t avail = (a.total_floats - first) * sizeof(float);
+        const int nrec = avail > 0xffffffffull ? (int)0xffffffffu : (int)(uint32_t)avail;
+        __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void *)(xp + first), (short)0, nrec, 0x00020000);
+        float *dst = buf + im * a.img_lds;
+        // Work units (channel cl, block b) are dealt round-robin to the waves.
+        int cl = 0, b = wave;
+        while (b >= nblk) {
+            b -= nblk;
+            ++cl;
+        }
+        while (cl < cn) {
+            const uint32_t voff = (uint32_t)((cl * plane + b * kStageBlock) * (int)sizeof(float)) + lane * 16;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(dst + cl * a.PLp + b * kStageBlock), 16, voff,
+                                                     0, 0, 0);
+            b += kS1Waves;
+            while (b >= nblk) {
+                b -= nblk;
+                ++cl;
+            }
+        }
+    }
+}
+
+// A window of up to 128 CSR entries of one row, decoded to LDS float indices:
+// lane l holds entries base+l (slot 0) and base+64+l (slot 1). Only the entries
+// of the current channel chunk are kept; they form a prefix of the window.
+struct Window {
+    int lo[2];
+    float w[2];
+    int n;
+};
+
+__device__ __forceinline__ Window load_window(const FwdArgs &a, const int32_t *__restrict__ offset,
+                                              const float *__restrict__ vals, int j, int e, int bound, int vb, int lane) {
+    Window win;
+    win.n = 0;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int idx = j + h * kWave + lane;
+        const bool valid = idx < e;
+        const int o = valid ? offset[idx] : 0x7fffffff;
+        const float w = valid ? vals[idx] : 0.0f;
+        const bool in = valid && o < bound;
+        const int c = (int)fast_div((uint32_t)o, a.magic, a.shift);
+        win.lo[h] = vb + o - c * a.plane_delta;
+        win.w[h] = w;
+        win.n += __builtin_popcountll(__builtin_amdgcn_ballot_w64(in));
+    }
+    return win;
+}
+
+template <int PI, int IPW>
+__device__ __forceinline__ void load_taps(float (&x)[IPW][PI], const float *lds, int ad, int img_lds) {
+#pragma unroll
+    for (int im = 0; im < IPW; ++im)
+#pragma unroll
+        for (int p = 0; p < PI; ++p) x[im][p] = lds[ad + im * img_lds + kWave * p];
+}
+
+template <int PI, int IPW>
+__device__ __forceinline__ void fma_taps(float (&acc)[IPW][PI], const float (&x)[IPW][PI], float v) {
+#pragma unroll
+    for (int im = 0; im < IPW; ++im)
+#pragma unroll
+        for (int p = 0; p < PI; ++p) acc[im][p] = fmaf(v, x[im][p], acc[im][p]);
+}
+
+__device__ __forceinline__ int lane_read_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ float lane_read_f(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+// Accumulate entries [0, n) of one window slot (n <= 64) into acc. Two-stage
+// software pipeline: the LDS reads of entry u+1 are in flight while the FMAs of
+// entry u issue. The loop body is branch-free so the accumulators and both
+// buffers keep their registers: past the last entry it re-reads that entry and
+// adds it with weight 0 (exact for finite inputs).
+template <int PI, int IPW>
+__device__ __forceinline__ void run_slot(float (&acc)[IPW][PI], int lo, float w, int n, const float *lds, int q,
+                                         int img_lds) {
+    if (n <= 0) return;
+    float x0[IPW][PI], x1[IPW][PI];
+    load_taps(x0, lds, lane_read_i(lo, 0) + q, img_lds);
+    // The scheduling barriers keep each refill after the FMAs that read the
+    // buffer it overwrites, so the two buffers alternate without copies.
+    for (int u = 0; u < n; u += 2) {
+        const int u1 = min(u + 1, n - 1), u2 = min(u + 2, n - 1);
+        const float w0 = lane_read_f(w, u);
+        const int w1_bits = lane_read_i(__float_as_int(w), u1);
+        const float w1 = __int_as_float((u + 1 < n) ? w1_bits : 0);
+        load_taps(x1, lds, lane_read_i(lo, u1) + q, img_lds);
+        fma_taps(acc, x0, w0);
+        __builtin_amdgcn_sched_barrier(0);
+        load_taps(x0, lds, lane_read_i(lo, u2) + q, img_lds);
+        fma_taps(acc, x1, w1);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+template <int PI, int IPW, int RPW, bool POOL>
+__global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2))) void spconv_s1_kernel(
+    FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ offset,
+    const float *__restrict__ vals, const float *__restrict__ bias, float *__restrict__ out) {
+    extern __shared__ float lds[];
+    constexpr int KT = RPW * kS1Waves;
+
+    const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
+    const int kt = L % a.nktiles;
+    const int grp = L / a.nktiles;
+    const int ty = grp % a.ntiles_y;
+    const int ig = grp / a.ntiles_y;
+    const int y0 = ty * a.TH;
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    const int lane = (int)threadIdx.x & 63;
+    const int kw = kt * KT + wave * RPW;  // first output channel of this wave
+    const int plane = a.Hp * a.Wp;
+
+    int cur[RPW], end[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+        const int k = kw + i;
+        cur[i] = (k < a.K) ? rowptr[k] : 0;
+        end[i] = (k < a.K) ? rowptr[k + 1] : 0;
+    }
+
+    float acc[RPW][IPW][PI];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i)
+#pragma unroll
+        for (int im = 0; im < IPW; ++im)
+#pragma unroll
+            for (int p = 0; p < PI; ++p) acc[i][im][p] = 0.0f;
+
+    // LDS float index of tap offset o for chunk ch, pixel q: vb(ch) + o - c*plane_delta + q.
+    auto vb_of = [&](int ch) { return (ch & 1) * a.buf_floats - ch * a.Cc * a.PLp; };
+    auto bound_of = [&](int ch) { return min((ch + 1) * a.Cc, a.C) * plane; };
+
+    Window win[RPW];
+    stage_chunk_s1(a, xp, lds, 0, ig, y0, wave, lane);
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) win[i] = load_window(a, offset, vals, cur[i], end[i], bound_of(0), vb_of(0), lane);
+    wait_async_copies();
+    __syncthreads();
+
+    for (int ch = 0; ch < a.nchunks; ++ch) {
+        if (ch + 1 < a.nchunks)
+            stage_chunk_s1(a, xp, lds + ((ch + 1) & 1) * a.buf_floats, ch + 1, ig, y0, wave, lane);
+        const int bound = bound_of(ch);
+        const int vb = vb_of(ch);
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            for (;;) {
+                const int n = win[i].n;
+                run_slot(acc[i], win[i].lo[0], win[i].w[0], min(n, kWave), lds, lane, a.img_lds);
+                run_slot(acc[i], win[i].lo[1], win[i].w[1], n - kWave, lds, lane, a.img_lds);
+                cur[i] += n;
+                if (n < 2 * kWave || cur[i] >= end[i]) break;
+                // The row has more entries in this chunk than one window holds.
+                win[i] = load_window(a, offset, vals, cur[i], end[i], bound, vb, lane);
+            }
+        }
+        if (ch + 1 < a.nchunks) {
+#pragma unroll
+            for (int i = 0; i < RPW; ++i)
+                win[i] = load_window(a, offset, vals, cur[i], end[i], bound_of(ch + 1), vb_of(ch + 1), lane);
+        }
+        wait_async_copies();
+        __syncthreads();  // chunk ch+1 is in LDS; every wave is done with chunk ch's buffer
+    }
+
+    const int tile_px = a.TH * a.Wp;
+    if constexpr (!POOL) {
+        int pix[PI];  // in-plane output index of each of this lane's pixels, or -1
+#pragma unroll
+        for (int p = 0; p < PI; ++p) {
+            const int q = lane + kWave * p;
+            const int yl = q / a.Wp, x = q - yl * a.Wp;
+            const int y = y0 + yl;
+            pix[p] = (q < tile_px && x < a.Wo && y < a.Ho) ? y * a.Wo + x : -1;
+        }
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int k = kw + i;
+            if (k >= a.K) break;
+            const float bk = bias ? bias[k] : 0.0f;
+#pragma unroll
+            for (int im = 0; im < IPW; ++im) {
+                const int n = ig * IPW + im;
+                if (n >= a.N) break;
+                float *op = out + ((size_t)n * a.K + k) * (size_t)a.Ho * a.Wo;
+#pragma unroll
+                for (int p = 0; p < PI; ++p) {
+                    float v = acc[i][im][p] + bk;
+                    if (a.relu) v = v > 0.0f ? v : 0.0f;
+                    if (pix[p] >= 0) op[pix[p]] = v;
+                }
+            }
+        }
+    } else {
+        // Each wave stages its own rows' activated tiles (all images) in LDS,
+        // then reduces 2x2 windows; no other wave touches that area. The last
+        // barrier of the chunk loop ordered these writes after every read of
+        // the input buffers.
+        constexpr int kImgPx = kWave * PI;
+        float *st = lds + wave * IPW * kImgPx;
+        const int prow0 = y0 / 2;
+        const int prows = a.TH / 2;
+        const int per_img = prows * a.Wq;
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int k = kw + i;
+            const float bk = (k < a.K && bias) ? bias[k] : 0.0f;
+            if (i > 0) __syncthreads();
+#pragma unroll
+            for (int im = 0; im < IPW; ++im)
+#pragma unroll
+                for (int p = 0; p < PI; ++p) {
+                    float v = acc[i][im][p] + bk;
+                    if (a.relu) v = v > 0.0f ? v : 0.0f;
+                    st[im * kImgPx + lane + kWave * p] = v;
+                }
+            __syncthreads();
+            if (k < a.K) {
+                for (int t = lane; t < IPW * per_img; t += kWave) {
+                    const int im = t / per_img;
+                    const int rem = t - im * per_img;
+                    const int r = rem / a.Wq;
+                    const int jq = rem - r * a.Wq;
+                    const int n = ig * IPW + im;
+                    const int pr = prow0 + r;
+                    if (n < a.N && pr < a.Hq) {
+                        const float *s0 = st + im * kImgPx + (2 * r) * a.Wp + 2 * jq;
+                        const float m = fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[a.Wp], s0[a.Wp + 1]));
+                        out[((size_t)n * a.K + k) * (size_t)a.Hq * a.Wq + (size_t)pr * a.Wq + jq] = m;
+                    }
+                }
+            }
+        }
+    }
+}
+
+// Generic-stride kernel: waves split the pixels of the tile and every wave
+// walks all KT rows; each pixel keeps its own LDS base (y*stride*Wp +
+// x*stride), so a nonzero costs one address add per pixel. Correct for any
+// stride; the stride-1 kernel above is the fast path.
+template <int P, int KT, bool POOL>
+__global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr,
+                                                         const int32_t *__restrict__ offset, const float *__restrict__ vals,
+                                                         const float *__restrict__ bias, float *__restrict__ out) {
     extern __shared__ float lds[];
 
     const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
@@ -141,28 +447,22 @@ __global__ __launch_bounds__(kThreads) void spconv_fwd_kernel(FwdArgs a) {
     const bool active = n < a.N;
     const int plane = a.Hp * a.Wp;
 
-    // CSR cursor per row of the tile (scalar registers).
     int cur[KT], end[KT];
 #pragma unroll
     for (int kk = 0; kk < KT; ++kk) {
         const int k = k0 + kk;
-        cur[kk] = (k < a.K) ? a.rowptr[k] : 0;
-        end[kk] = (k < a.K) ? a.rowptr[k + 1] : 0;
+        cur[kk] = (k < a.K) ? rowptr[k] : 0;
+        end[kk] = (k < a.K) ? rowptr[k + 1] : 0;
     }
 
-    // Pixels of this lane inside the image tile: q = qw + 64*j.
     const int qw = wseg * kWave * P + lane;
     const int tile_px = a.TH * a.wv;
-    int base[S1 ? 1 : P];
-    if constexpr (S1) {
-        base[0] = qw;
-    } else {
+    int base[P];
 #pragma unroll
-        for (int j = 0; j < P; ++j) {
-            const int q = qw + kWave * j;
-            const int yl = q / a.Wo, x = q - yl * a.Wo;
-            base[j] = (q < tile_px) ? yl * a.stride * a.Wp + x * a.stride : 0;
-        }
+    for (int j = 0; j < P; ++j) {
+        const int q = qw + kWave * j;
+        const int yl = q / a.Wo, x = q - yl * a.Wo;
+        base[j] = (q < tile_px) ? yl * a.stride * a.Wp + x * a.stride : 0;
     }
 
     float acc[KT][P];
@@ -178,59 +478,25 @@ __global__ __launch_bounds__(kThreads) void spconv_fwd_kernel(FwdArgs a) {
         const int c0 = ch * a.Cc;
         const int cn = min(a.Cc, a.C - c0);
         __syncthreads();  // every wave is done with the previous chunk
-        for (int im = 0; im < a.ipw; ++im) {
-            const int nn = ig * a.ipw + im;
-            if (nn >= a.N) break;
-            for (int cl = 0; cl < cn; ++cl) {
-                const float *src = a.xp + ((size_t)(nn * a.C + c0 + cl) * a.Hp + in_row0) * a.Wp;
-                float *dst = lds + im * a.img_lds + cl * a.PL;
-                for (int e = (int)threadIdx.x; e < seg_len; e += kThreads) dst[e] = src[e];
-            }
-        }
+        stage_chunk(a, xp, lds, ch, ig, in_row0, seg_len, wave, lane);
+        wait_async_copies();
         __syncthreads();
         if (!active) continue;
 
-        // LDS address of tap `off` for pixel base b: vb + off - c*plane_delta + b,
-        // where c = off / plane is the tap's channel.
         const int vb = img * a.img_lds - c0 * a.PL;
         const int bound = (c0 + cn) * plane;
 #pragma unroll
         for (int kk = 0; kk < KT; ++kk) {
             int j = cur[kk];
             const int e = end[kk];
-            while (j + 8 <= e) {
-                int o[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) o[u] = a.offset[j + u];
-                if (o[7] >= bound) break;
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const float v = a.vals[j + u];
-                    const int c = (int)fast_div((uint32_t)o[u], a.magic, a.shift);
-                    const int ad = vb + o[u] - c * a.plane_delta;
-                    if constexpr (S1) {
-#pragma unroll
-                        for (int p = 0; p < P; ++p) acc[kk][p] = fmaf(v, lds[ad + base[0] + kWave * p], acc[kk][p]);
-                    } else {
-#pragma unroll
-                        for (int p = 0; p < P; ++p) acc[kk][p] = fmaf(v, lds[ad + base[p]], acc[kk][p]);
-                    }
-                }
-                j += 8;
-            }
             while (j < e) {
-                const int o = a.offset[j];
+                const int o = offset[j];
                 if (o >= bound) break;
-                const float v = a.vals[j];
+                const float v = vals[j];
                 const int c = (int)fast_div((uint32_t)o, a.magic, a.shift);
                 const int ad = vb + o - c * a.plane_delta;
-                if constexpr (S1) {
 #pragma unroll
-                    for (int p = 0; p < P; ++p) acc[kk][p] = fmaf(v, lds[ad + base[0] + kWave * p], acc[kk][p]);
-                } else {
-#pragma unroll
-                    for (int p = 0; p < P; ++p) acc[kk][p] = fmaf(v, lds[ad + base[p]], acc[kk][p]);
-                }
+                for (int p = 0; p < P; ++p) acc[kk][p] = fmaf(v, lds[ad + base[p]], acc[kk][p]);
                 ++j;
             }
             cur[kk] = j;
@@ -239,7 +505,7 @@ __global__ __launch_bounds__(kThreads) void spconv_fwd_kernel(FwdArgs a) {
 
     if constexpr (!POOL) {
         if (!active) return;
-        int pix[P];  // in-plane output index of each of this lane's pixels, or -1
+        int pix[P];
 #pragma unroll
         for (int j = 0; j < P; ++j) {
             const int q = qw + kWave * j;
@@ -251,8 +517,8 @@ __global__ __launch_bounds__(kThreads) void spconv_fwd_kernel(FwdArgs a) {
         for (int kk = 0; kk < KT; ++kk) {
             const int k = k0 + kk;
             if (k >= a.K) break;
-            const float bk = a.bias ? a.bias[k] : 0.0f;
-            float *op = a.out + ((size_t)n * a.K + k) * (size_t)a.Ho * a.Wo;
+            const float bk = bias ? bias[k] : 0.0f;
+            float *op = out + ((size_t)n * a.K + k) * (size_t)a.Ho * a.Wo;
 #pragma unroll
             for (int j = 0; j < P; ++j) {
                 float v = acc[kk][j] + bk;
@@ -261,7 +527,6 @@ __global__ __launch_bounds__(kThreads) void spconv_fwd_kernel(FwdArgs a) {
             }
         }
     } else {
-        // Stage each row's activated tile in LDS, then reduce 2x2 windows.
         const int img_px = a.wpi * kWave * P;
         const int prow0 = y0 / 2;
         const int prows = a.TH / 2;
@@ -271,7 +536,7 @@ __global__ __launch_bounds__(kThreads) void spconv_fwd_kernel(FwdArgs a) {
         for (int kk = 0; kk < KT; ++kk) {
             const int k = k0 + kk;
             if (k >= a.K) break;
-            const float bk = a.bias ? a.bias[k] : 0.0f;
+            const float bk = bias ? bias[k] : 0.0f;
             __syncthreads();  // previous readers of the staging area are done
 #pragma unroll
             for (int j = 0; j < P; ++j) {
@@ -290,7 +555,7 @@ __global__ __launch_bounds__(kThreads) void spconv_fwd_kernel(FwdArgs a) {
                 if (nn < a.N && pi < a.Hq) {
                     const float *s0 = lds + im * img_px + (2 * i) * a.wv + 2 * jq;
                     const float m = fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[a.wv], s0[a.wv + 1]));
-                    a.out[((size_t)nn * a.K + k) * (size_t)a.Hq * a.Wq + (size_t)pi * a.Wq + jq] = m;
+                    out[((size_t)nn * a.K + k) * (size_t)a.Hq * a.Wq + (size_t)pi * a.Wq + jq] = m;
                 }
             }
         }
@@ -323,80 +588,89 @@ bool div_magic(uint32_t d, uint32_t *magic, int *shift) {
 
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+enum class Kind { kStride1, kGeneric };
+
 struct Plan {
-    int P = 0, KT = 0;
-    bool s1 = true;
-    int TH = 0, ntiles_y = 0, ipw = 0, wpi = 0, Cc = 0, nchunks = 0, rows_in = 0, PL = 0, img_lds = 0, wv = 0;
-    int nktiles = 0, total_wgs = 0;
+    Kind kind = Kind::kStride1;
+    int PI = 0, IPW = 0, RPW = 0;  // stride-1 kernel
+    int P = 0, KT = 0;             // generic kernel
+    int TH = 0, ntiles_y = 0, ipw = 0, wpi = 0, Cc = 0, nchunks = 0, rows_in = 0, PL = 0, PLp = 0, img_lds = 0;
+    int buf_floats = 0, wv = 0, rows_per_wg = 0, nktiles = 0, total_wgs = 0;
     size_t lds_bytes = 0;
 };
 
-// Picks the pixels per lane (P), the waves per image and the tile height that
-// waste the fewest lanes, then the channel chunk that fits the LDS budget.
-bool make_plan(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int stride, int R, int S, bool pool, Plan *out) {
-    const bool s1 = stride == 1;
-    const int wv = s1 ? Wp : Wo;
-    const int img_pix = Ho * wv;
-    static const int kP_s1[] = {8, 7, 6, 5, 4};
-    static const int kP_gen[] = {4};
-    const int *Ps = s1 ? kP_s1 : kP_gen;
-    const int nP = s1 ? 5 : 1;
+// Pixels per lane per image (PI) and images per workgroup (IPW) the stride-1
+// kernel is built for.
+constexpr int kPiSingle[] = {32, 30, 28, 26, 24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4};
+constexpr int kPiMulti[] = {8, 6, 4, 2};
+
+bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, int S, bool pool, Plan *out) {
+    const int img_pix = Ho * Wp;
     Plan best;
-    double best_eff = -1.0;
-    for (int pi = 0; pi < nP; ++pi) {
-        const int P = Ps[pi];
-        for (int wpi : {4, 2, 1}) {
-            const int ipw = kWaves / wpi;
-            const int cap = wpi * kWave * P;  // virtual pixels per image tile
-            int TH, nt;
-            if (img_pix <= cap) {
-                TH = Ho;
-                nt = 1;
-            } else {
-                if (ipw != 1) continue;  // several images per workgroup only when each fits whole
-                int th_max = cap / wv;
-                if (pool) th_max &= ~1;
-                if (th_max < 1) continue;
-                nt = ceil_div(Ho, th_max);
-                TH = ceil_div(Ho, nt);
-                if (pool && (TH & 1)) ++TH;
-                nt = ceil_div(Ho, TH);
-            }
-            const int rows_in = (TH - 1) * stride + R;
-            const int PL = rows_in * Wp;
-            const int slack = s1 ? (cap - TH * Wp) + S : 0;
-            int cc_max = (kLdsBudgetFloats - slack) / (ipw * PL);
-            if (cc_max < 1) continue;
-            cc_max = std::min(cc_max, C);
-            const int nchunks = ceil_div(C, cc_max);
-            const int Cc = ceil_div(C, nchunks);
-            const double eff = (double)Ho * Wo / ((double)nt * ipw * cap / ipw);
-            // Prefer the least waste; on ties, more pixels per lane.
-            if (eff > best_eff + 1e-9) {
-                best_eff = eff;
-                best.P = P;
-                best.s1 = s1;
-                best.TH = TH;
-                best.ntiles_y = nt;
-                best.ipw = ipw;
-                best.wpi = wpi;
-                best.Cc = Cc;
-                best.nchunks = nchunks;
-                best.rows_in = rows_in;
-                best.PL = PL;
-                best.img_lds = Cc * PL;
-                best.wv = wv;
-                size_t floats = (size_t)ipw * Cc * PL + (size_t)slack;
-                if (pool) floats = std::max(floats, (size_t)ipw * cap);
-                best.lds_bytes = floats * sizeof(float);
-            }
+    double best_score = -1.0;
+    auto consider = [&](int PI, int IPW) {
+        const int cap = kWave * PI;  // virtual pixels per image tile
+        int TH, nt;
+        if (img_pix <= cap) {
+            TH = Ho;
+            nt = 1;
+        } else {
+            if (IPW != 1) return;
+            int th_max = cap / Wp;
+            if (pool) th_max &= ~1;
+            if (th_max < 1) return;
+            nt = ceil_div(Ho, th_max);
+            TH = ceil_div(Ho, nt);
+            if (pool && (TH & 1)) ++TH;
+            nt = ceil_div(Ho, TH);
         }
-    }
-    if (best_eff < 0) return false;
-    const int groups = ceil_div(N, best.ipw) * best.ntiles_y;
-    best.KT = (groups * ceil_div(K, 8) >= 512) ? 8 : 4;
-    if (!s1) best.KT = 4;
-    best.nktiles = ceil_div(K, best.KT);
+        const int rows_in = TH + R - 1;
+        const int PL = rows_in * Wp;
+        const int PLp = ceil_div(PL, kStageBlock) * kStageBlock;
+        // Lanes past the tile read up to cap - TH*Wp + S - 2 floats beyond the
+        // last image block; keep that inside the buffer.
+        const int slack = cap - TH * Wp + S;
+        const int per_buf = kS1LdsFloats / 2;
+        int cc_max = (per_buf - slack) / (IPW * PLp);
+        if (cc_max < 1) return;
+        cc_max = std::min(cc_max, C);
+        const int nchunks = ceil_div(C, cc_max);
+        const int Cc = ceil_div(C, nchunks);
+        // The DMA offsets of one chunk are 32-bit byte offsets.
+        if (((long long)(Cc - 1) * Hp * Wp + PLp) * 4 >= (1LL << 32)) return;
+        const double eff = (double)Ho * Wo / ((double)nt * cap);
+        // Fewest idle lanes first; then more pixels per lane and fewer chunks.
+        const double score = eff * (1.0 + 0.002 * PI * IPW) / (1.0 + 0.001 * nchunks);
+        if (score > best_score) {
+            best_score = score;
+            best.kind = Kind::kStride1;
+            best.PI = PI;
+            best.IPW = IPW;
+            best.TH = TH;
+            best.ntiles_y = nt;
+            best.ipw = IPW;
+            best.Cc = Cc;
+            best.nchunks = nchunks;
+            best.rows_in = rows_in;
+            best.PL = PL;
+            best.PLp = PLp;
+            best.img_lds = Cc * PLp;
+            best.buf_floats = ceil_div(IPW * Cc * PLp + slack, 64) * 64;
+            best.wv = Wp;
+            size_t floats = 2 * (size_t)best.buf_floats;
+            if (pool) floats = std::max(floats, (size_t)kS1Waves * IPW * cap);
+            best.lds_bytes = floats * sizeof(float);
+        }
+    };
+    for (int PI : kPiSingle) consider(PI, 1);
+    for (int IPW : {2, 4})
+        if (IPW <= N)
+            for (int PI : kPiMulti) consider(PI, IPW);
+    if (best_score < 0) return false;
+    const int groups = ceil_div(N, best.IPW) * best.ntiles_y;
+    best.RPW = (groups * ceil_div(K, 2 * kS1Waves) >= 256) ? 2 : 1;
+    best.rows_per_wg = best.RPW * kS1Waves;
+    best.nktiles = ceil_div(K, best.rows_per_wg);
     const long long wgs = (long long)groups * best.nktiles;
     if (wgs > 0x7fffffffLL) return false;
     best.total_wgs = (int)wgs;
@@ -404,26 +678,93 @@ bool make_plan(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int stride, 
     return true;
 }
 
-using FwdKernel = void (*)(FwdArgs);
-
-template <int P, int KT, bool S1>
-FwdKernel pick_pool(bool pool) {
-    return pool ? spconv_fwd_kernel<P, KT, S1, true> : spconv_fwd_kernel<P, KT, S1, false>;
+bool plan_generic(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int stride, int R, bool pool, Plan *out) {
+    constexpr int P = 4, KT = 4;
+    const int wv = Wo;
+    const int img_pix = Ho * wv;
+    Plan best;
+    double best_eff = -1.0;
+    for (int wpi : {4, 2, 1}) {
+        const int ipw = kWaves / wpi;
+        const int cap = wpi * kWave * P;
+        int TH, nt;
+        if (img_pix <= cap) {
+            TH = Ho;
+            nt = 1;
+        } else {
+            if (ipw != 1) continue;
+            int th_max = cap / wv;
+            if (pool) th_max &= ~1;
+            if (th_max < 1) continue;
+            nt = ceil_div(Ho, th_max);
+            TH = ceil_div(Ho, nt);
+            if (pool && (TH & 1)) ++TH;
+            nt = ceil_div(Ho, TH);
+        }
+        const int rows_in = (TH - 1) * stride + R;
+        const int PL = rows_in * Wp;
+        int cc_max = kLdsBudgetFloats / (ipw * PL);
+        if (cc_max < 1) continue;
+        cc_max = std::min(cc_max, C);
+        const int nchunks = ceil_div(C, cc_max);
+        const int Cc = ceil_div(C, nchunks);
+        const double eff = (double)Ho * Wo / ((double)nt * cap);
+        if (eff > best_eff + 1e-9) {
+            best_eff = eff;
+            best.kind = Kind::kGeneric;
+            best.P = P;
+            best.KT = KT;
+            best.TH = TH;
+            best.ntiles_y = nt;
+            best.ipw = ipw;
+            best.wpi = wpi;
+            best.Cc = Cc;
+            best.nchunks = nchunks;
+            best.rows_in = rows_in;
+            best.PL = PL;
+            best.img_lds = Cc * PL;
+            best.buf_floats = ipw * Cc * PL;
+            best.wv = wv;
+            size_t floats = (size_t)best.buf_floats;
+            if (pool) floats = std::max(floats, (size_t)ipw * cap);
+            best.lds_bytes = floats * sizeof(float);
+        }
+    }
+    if (best_eff < 0) return false;
+    const int groups = ceil_div(N, best.ipw) * best.ntiles_y;
+    best.rows_per_wg = KT;
+    best.nktiles = ceil_div(K, KT);
+    const long long wgs = (long long)groups * best.nktiles;
+    if (wgs > 0x7fffffffLL) return false;
+    best.total_wgs = (int)wgs;
+    *out = best;
+    return true;
 }
 
-template <int P>
-FwdKernel pick_kt(int KT, bool pool) {
-    return KT == 8 ? pick_pool<P, 8, true>(pool) : pick_pool<P, 4, true>(pool);
+using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_t *, const float *,
+                           const float *, float *);
+
+template <int PI, int IPW>
+FwdKernel pick_s1_rpw(int RPW, bool pool) {
+    if (RPW == 2) return pool ? spconv_s1_kernel<PI, IPW, 2, true> : spconv_s1_kernel<PI, IPW, 2, false>;
+    return pool ? spconv_s1_kernel<PI, IPW, 1, true> : spconv_s1_kernel<PI, IPW, 1, false>;
+}
+
+template <int IPW, int... PIs>
+FwdKernel pick_s1_pi(int PI, int RPW, bool pool) {
+    FwdKernel k = nullptr;
+    ((PI == PIs ? (k = pick_s1_rpw<PIs, IPW>(RPW, pool), 0) : 0), ...);
+    return k;
 }
 
 FwdKernel pick_kernel(const Plan &pl, bool pool) {
-    if (!pl.s1) return pick_pool<4, 4, false>(pool);
-    switch (pl.P) {
-        case 8: return pick_kt<8>(pl.KT, pool);
-        case 7: return pick_kt<7>(pl.KT, pool);
-        case 6: return pick_kt<6>(pl.KT, pool);
-        case 5: return pick_kt<5>(pl.KT, pool);
-        case 4: return pick_kt<4>(pl.KT, pool);
+    if (pl.kind == Kind::kGeneric)
+        return pool ? spconv_generic_kernel<4, 4, true> : spconv_generic_kernel<4, 4, false>;
+    switch (pl.IPW) {
+        case 1:
+            return pick_s1_pi<1, 32, 30, 28, 26, 24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4>(pl.PI, pl.RPW, pool);
+        case 2: return pick_s1_pi<2, 8, 6, 4, 2>(pl.PI, pl.RPW, pool);
+        case 4: return pick_s1_pi<4, 8, 6, 4, 2>(pl.PI, pl.RPW, pool);
         default: return nullptr;
     }
 }
@@ -505,14 +846,10 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     if (pool && (Ho < 2 || Wo < 2)) return SPCONV_EINVAL;
 
     Plan pl;
-    if (!make_plan(N, C, K, (int)Hp, (int)Wp, Ho, Wo, stride, R, S, pool, &pl)) return SPCONV_EINVAL;
+    const bool ok = (stride == 1) ? plan_stride1(N, C, K, (int)Hp, (int)Wp, Ho, Wo, R, S, pool, &pl)
+                                  : plan_generic(N, C, K, (int)Hp, (int)Wp, Ho, Wo, stride, R, pool, &pl);
+    if (!ok) return SPCONV_EINVAL;
     FwdArgs a;
-    a.xp = in_padded;
-    a.rowptr = csr->rowptr;
-    a.offset = csr->offset;
-    a.vals = csr->vals;
-    a.bias = bias;
-    a.out = out;
     a.N = N;
     a.C = C;
     a.K = K;
@@ -523,6 +860,7 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     a.Hq = pool ? Ho / 2 : Ho;
     a.Wq = pool ? Wo / 2 : Wo;
     a.stride = stride;
+    a.nnz = (int)csr->nnz;
     a.relu = (flags & SPCONV_RELU) ? 1 : 0;
     a.TH = pl.TH;
     a.ntiles_y = pl.ntiles_y;
@@ -534,12 +872,22 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     a.rows_in = pl.rows_in;
     a.PL = pl.PL;
     a.img_lds = pl.img_lds;
+    a.buf_floats = pl.buf_floats;
+    a.PLp = pl.PLp;
+    a.total_floats = (size_t)N * C * Hp * Wp;
     a.wv = pl.wv;
     a.total_wgs = pl.total_wgs;
     if (!div_magic((uint32_t)(Hp * Wp), &a.magic, &a.shift)) return SPCONV_EINVAL;
-    a.plane_delta = (int)(Hp * Wp) - pl.PL;
+    // Both kernels address a staged channel at its LDS pitch: PLp (stride 1) or PL.
+    a.plane_delta = (int)(Hp * Wp) - (pl.kind == Kind::kStride1 ? pl.PLp : pl.PL);
     FwdKernel kern = pick_kernel(pl, pool);
     if (!kern) return SPCONV_EINVAL;
-    hipLaunchKernelGGL(kern, dim3((unsigned)pl.total_wgs), dim3(kThreads), pl.lds_bytes, stream, a);
+    const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
+    if (pl.lds_bytes > 65536 &&
+        hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds_bytes) !=
+            hipSuccess)
+        return SPCONV_EHIP;
+    hipLaunchKernelGGL(kern, dim3((unsigned)pl.total_wgs), dim3(threads), pl.lds_bytes, stream, a, in_padded,
+                       csr->rowptr, csr->offset, csr->vals, bias, out);
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
