@@ -17,8 +17,6 @@ LIB_PATH = Path(__file__).resolve().parent / "libspconv.so"
 if not LIB_PATH.exists():
     raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2005_04091_amd.build` first")
 
-_lib = ctypes.CDLL(str(LIB_PATH))
-
 SPCONV_OK = 0
 SPCONV_EINVAL = -1
 SPCONV_ECAPACITY = -2
@@ -39,19 +37,27 @@ class spconv_csr(ctypes.Structure):
 
 _c_int = ctypes.c_int
 _vp = ctypes.c_void_p
-_lib.spconv_pack_csr.restype = _c_int
-_lib.spconv_pack_csr.argtypes = [_vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp, _vp,
-                                 ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
-_lib.spconv_pad_input.restype = _c_int
-_lib.spconv_pad_input.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp]
-_lib.spconv_forward.restype = _c_int
-_lib.spconv_forward.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int,
-                                _c_int, _c_int, _c_int, _vp, ctypes.c_uint32, _vp, _vp]
-_lib.spconv_output_shape.restype = _c_int
-_lib.spconv_output_shape.argtypes = [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_uint32,
-                                     ctypes.POINTER(_c_int), ctypes.POINTER(_c_int)]
-_lib.spconv_strerror.restype = ctypes.c_char_p
-_lib.spconv_strerror.argtypes = [_c_int]
+
+
+def _bind(lib):
+    """Declare the C signatures on a loaded libspconv.so and return it."""
+    lib.spconv_pack_csr.restype = _c_int
+    lib.spconv_pack_csr.argtypes = [_vp, _vp, _c_int, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp, _vp, _vp,
+                                    ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
+    lib.spconv_pad_input.restype = _c_int
+    lib.spconv_pad_input.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp]
+    lib.spconv_forward.restype = _c_int
+    lib.spconv_forward.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int,
+                                   _c_int, _c_int, _c_int, _vp, ctypes.c_uint32, _vp, _vp]
+    lib.spconv_output_shape.restype = _c_int
+    lib.spconv_output_shape.argtypes = [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_uint32,
+                                        ctypes.POINTER(_c_int), ctypes.POINTER(_c_int)]
+    lib.spconv_strerror.restype = ctypes.c_char_p
+    lib.spconv_strerror.argtypes = [_c_int]
+    return lib
+
+
+_lib = _bind(ctypes.CDLL(str(LIB_PATH)))
 
 
 class SpconvError(RuntimeError):
