@@ -30,6 +30,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstring>
 
@@ -203,28 +204,52 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
     }
 }
 
-// A window of up to 128 CSR entries of one row, decoded to LDS float indices:
-// lane l holds entries base+l (slot 0) and base+64+l (slot 1). Only the entries
-// of the current channel chunk are kept; they form a prefix of the window.
+// Up to 128 consecutive CSR entries of one row as loaded: lane l holds entries
+// base+l (slot 0) and base+64+l (slot 1); entries at or past the row's end read
+// as offset INT32_MAX, weight 0.
+struct RawWindow {
+    int o[2];
+    float w[2];
+    int base;
+};
+
+__device__ __forceinline__ RawWindow fetch_window(const int32_t *__restrict__ offset, const float *__restrict__ vals,
+                                                  int j, int e, int lane) {
+    RawWindow r;
+    r.base = j;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int idx = j + h * kWave + lane;
+        const bool valid = idx < e;
+        r.o[h] = valid ? offset[idx] : 0x7fffffff;
+        r.w[h] = valid ? vals[idx] : 0.0f;
+    }
+    return r;
+}
+
+// A window decoded for one channel chunk: LDS float indices of its entries and
+// the number n of them that belong to the chunk (a prefix of the window).
 struct Window {
     int lo[2];
     float w[2];
     int n;
 };
 
-__device__ __forceinline__ Window load_window(const FwdArgs &a, const int32_t *__restrict__ offset,
-                                              const float *__restrict__ vals, int j, int e, int bound, int vb, int lane) {
+__device__ __forceinline__ Window decode_window(const FwdArgs &a, const RawWindow &r, int e, int bound, int vb,
+                                                int lane) {
     Window win;
     win.n = 0;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-        const int idx = j + h * kWave + lane;
-        const bool valid = idx < e;
-        const int o = valid ? offset[idx] : 0x7fffffff;
-        const float w = valid ? vals[idx] : 0.0f;
-        const bool in = valid && o < bound;
+        const int o = r.o[h];
+        const bool in = r.base + h * kWave + lane < e && o < bound;
         const int c = (int)fast_div((uint32_t)o, a.magic, a.shift);
         win.lo[h] = vb + o - c * a.plane_delta;
+        // Touch the loaded weight here, so that the wait for its load is
+        // placed at this decode and not deferred into the compute loop, where
+        // it would also wait for the chunk copies in flight.
+        float w = r.w[h];
+        asm volatile("" : "+v"(w));
         win.w[h] = w;
         win.n += __builtin_popcountll(__builtin_amdgcn_ballot_w64(in));
     }
@@ -284,23 +309,45 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2
     FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ offset,
     const float *__restrict__ vals, const float *__restrict__ bias, float *__restrict__ out) {
     extern __shared__ float lds[];
-    constexpr int KT = RPW * kS1Waves;
+    constexpr int KT = RPW * kS1Waves;  // output channels per workgroup
 
     const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
-    const int kt = L % a.nktiles;
-    const int grp = L / a.nktiles;
-    const int ty = grp % a.ntiles_y;
-    const int ig = grp / a.ntiles_y;
-    const int y0 = ty * a.TH;
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int lane = (int)threadIdx.x & 63;
-    const int kw = kt * KT + wave * RPW;  // first output channel of this wave
+    const int kt = L % a.nktiles;
+    const int tile = L / a.nktiles;
+    const int ty = tile % a.ntiles_y;
+    const int ig = tile / a.ntiles_y;
+    const int y0 = ty * a.TH;
     const int plane = a.Hp * a.Wp;
 
+    // Output channels of this wave. With RPW > 1 the workgroup's KT channels
+    // are ranked by nonzero count and dealt to the waves in snake order (ranks
+    // w, 2*8-1-w, 2*8+w, ...), so heavy and light channels share a wave and the
+    // waves' loads even out.
+    int krow[RPW];
+    if constexpr (RPW == 1) {
+        krow[0] = kt * KT + wave;
+    } else {
+        const int k0 = kt * KT;
+        int nz = -1;
+        if (lane < KT && k0 + lane < a.K) nz = rowptr[k0 + lane + 1] - rowptr[k0 + lane];
+        int rank = 0;
+        for (int j = 0; j < KT; ++j) {
+            const int o = __builtin_amdgcn_readlane(nz, j);
+            rank += (o > nz || (o == nz && j < lane)) ? 1 : 0;
+        }
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int want = i * kS1Waves + ((i & 1) ? kS1Waves - 1 - wave : wave);
+            const unsigned long long m = __builtin_amdgcn_ballot_w64(lane < KT && rank == want);
+            krow[i] = k0 + (int)__builtin_ctzll(m);
+        }
+    }
     int cur[RPW], end[RPW];
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
-        const int k = kw + i;
+        const int k = krow[i];
         cur[i] = (k < a.K) ? rowptr[k] : 0;
         end[i] = (k < a.K) ? rowptr[k + 1] : 0;
     }
@@ -318,15 +365,25 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2
     auto bound_of = [&](int ch) { return min((ch + 1) * a.Cc, a.C) * plane; };
 
     Window win[RPW];
+    RawWindow next[RPW];
     stage_chunk_s1(a, xp, lds, 0, ig, y0, wave, lane);
 #pragma unroll
-    for (int i = 0; i < RPW; ++i) win[i] = load_window(a, offset, vals, cur[i], end[i], bound_of(0), vb_of(0), lane);
+    for (int i = 0; i < RPW; ++i) {
+        next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
+        win[i] = decode_window(a, next[i], end[i], bound_of(0), vb_of(0), lane);
+    }
     wait_async_copies();
     __syncthreads();
 
     for (int ch = 0; ch < a.nchunks; ++ch) {
-        if (ch + 1 < a.nchunks)
+        const bool more = ch + 1 < a.nchunks;
+        if (more) {
             stage_chunk_s1(a, xp, lds + ((ch + 1) & 1) * a.buf_floats, ch + 1, ig, y0, wave, lane);
+            // Fetch the next chunk's windows now, from where this chunk's
+            // entries end, so their latency hides behind this chunk's work.
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) next[i] = fetch_window(offset, vals, cur[i] + win[i].n, end[i], lane);
+        }
         const int bound = bound_of(ch);
         const int vb = vb_of(ch);
 #pragma unroll
@@ -338,16 +395,24 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2
                 cur[i] += n;
                 if (n < 2 * kWave || cur[i] >= end[i]) break;
                 // The row has more entries in this chunk than one window holds.
-                win[i] = load_window(a, offset, vals, cur[i], end[i], bound, vb, lane);
+                win[i] = decode_window(a, fetch_window(offset, vals, cur[i], end[i], lane), end[i], bound, vb, lane);
             }
         }
-        if (ch + 1 < a.nchunks) {
+        if (more) {
 #pragma unroll
-            for (int i = 0; i < RPW; ++i)
-                win[i] = load_window(a, offset, vals, cur[i], end[i], bound_of(ch + 1), vb_of(ch + 1), lane);
+            for (int i = 0; i < RPW; ++i) {
+                // A row that overflowed a window in this chunk ends elsewhere.
+                if (next[i].base != cur[i]) next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
+                win[i] = decode_window(a, next[i], end[i], bound_of(ch + 1), vb_of(ch + 1), lane);
+            }
         }
-        wait_async_copies();
-        __syncthreads();  // chunk ch+1 is in LDS; every wave is done with chunk ch's buffer
+        // Chunk ch+1 is in LDS and every wave is done with chunk ch's buffer.
+        // After the last chunk only the pooled epilogue, which reuses the
+        // buffers, needs the barrier.
+        if (POOL || more) {
+            wait_async_copies();
+            __syncthreads();
+        }
     }
 
     const int tile_px = a.TH * a.Wp;
@@ -362,8 +427,8 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2
         }
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
-            const int k = kw + i;
-            if (k >= a.K) break;
+            const int k = krow[i];
+            if (k >= a.K) continue;
             const float bk = bias ? bias[k] : 0.0f;
 #pragma unroll
             for (int im = 0; im < IPW; ++im) {
@@ -390,7 +455,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2
         const int per_img = prows * a.Wq;
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
-            const int k = kw + i;
+            const int k = krow[i];
             const float bk = (k < a.K && bias) ? bias[k] : 0.0f;
             if (i > 0) __syncthreads();
 #pragma unroll
@@ -599,16 +664,63 @@ struct Plan {
     size_t lds_bytes = 0;
 };
 
-// Pixels per lane per image (PI) and images per workgroup (IPW) the stride-1
-// kernel is built for.
-constexpr int kPiSingle[] = {32, 30, 28, 26, 24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4};
+using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_t *, const float *, const float *,
+                          float *);
+
+template <int PI, int IPW>
+FwdKernel pick_s1_rpw(int RPW, bool pool) {
+    // Accumulators per lane: RPW * IPW * PI, kept at or below 64.
+    if constexpr (PI * IPW <= 16)
+        if (RPW == 4) return pool ? spconv_s1_kernel<PI, IPW, 4, true> : spconv_s1_kernel<PI, IPW, 4, false>;
+    if constexpr (PI * IPW <= 32)
+        if (RPW == 2) return pool ? spconv_s1_kernel<PI, IPW, 2, true> : spconv_s1_kernel<PI, IPW, 2, false>;
+    if (RPW == 1) return pool ? spconv_s1_kernel<PI, IPW, 1, true> : spconv_s1_kernel<PI, IPW, 1, false>;
+    return nullptr;
+}
+
+template <int IPW, int... PIs>
+FwdKernel pick_s1_pi(int PI, int RPW, bool pool) {
+    FwdKernel k = nullptr;
+    ((PI == PIs ? (k = pick_s1_rpw<PIs, IPW>(RPW, pool), 0) : 0), ...);
+    return k;
+}
+
+// Pixels per lane per image (PI), images per wave (IPW) and channels per wave
+// (RPW) the stride-1 kernel is built for.
+constexpr int kPiSingle[] = {32, 30, 28, 26, 24, 22, 20, 18, 16, 14, 13, 12, 11, 10, 9, 8, 7, 6, 5, 4};
 constexpr int kPiMulti[] = {8, 6, 4, 2};
 
-bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, int S, bool pool, Plan *out) {
+FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool) {
+    switch (IPW) {
+        case 1:
+            return pick_s1_pi<1, 32, 30, 28, 26, 24, 22, 20, 18, 16, 14, 13, 12, 11, 10, 9, 8, 7, 6, 5, 4>(PI, RPW,
+                                                                                                          pool);
+        case 2: return pick_s1_pi<2, 8, 6, 4, 2>(PI, RPW, pool);
+        case 4: return pick_s1_pi<4, 8, 6, 4, 2>(PI, RPW, pool);
+        default: return nullptr;
+    }
+}
+
+// Picks the stride-1 tiling with the smallest modelled run time. The model
+// counts LDS cycles: every nonzero costs a wave IPW*PI LDS reads (2 cycles
+// each, 64 lanes x 4 bytes at 128 bytes per cycle) plus about three reads'
+// worth of issue overhead (weight and offset broadcast, address add, loop
+// control; fitted to measured rates at 7 to 32 pixels per lane), and the 8
+// waves of a workgroup share one LDS. Per chunk, the workgroup waits for its
+// slowest wave: with m nonzeros per wave and chunk (binomial counts), the
+// expected maximum over 8 waves exceeds the mean by about 1.42 * sqrt(m).
+// Each chunk adds a fixed cost (barrier, pipeline refill) and the LDS writes
+// of its copy, halo rows included; the pooled epilogue adds two barriers per
+// channel of a wave. Workgroups run one per CU, in rounds of 256.
+bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, int S, bool pool, long long nnz,
+                  Plan *out) {
     const int img_pix = Ho * Wp;
+    const double row_nnz = std::max(1.0, (double)nnz / K);
+    const double density = std::max(1e-3, (double)nnz / ((double)K * C * R * S));
     Plan best;
-    double best_score = -1.0;
-    auto consider = [&](int PI, int IPW) {
+    double best_time = -1.0;
+    auto consider = [&](int PI, int IPW, int RPW) {
+        if (!pick_s1(PI, IPW, RPW, pool)) return;
         const int cap = kWave * PI;  // virtual pixels per image tile
         int TH, nt;
         if (img_pix <= cap) {
@@ -638,14 +750,20 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, in
         const int Cc = ceil_div(C, nchunks);
         // The DMA offsets of one chunk are 32-bit byte offsets.
         if (((long long)(Cc - 1) * Hp * Wp + PLp) * 4 >= (1LL << 32)) return;
-        const double eff = (double)Ho * Wo / ((double)nt * cap);
-        // Fewest idle lanes first; then more pixels per lane and fewer chunks.
-        const double score = eff * (1.0 + 0.002 * PI * IPW) / (1.0 + 0.001 * nchunks);
-        if (score > best_score) {
-            best_score = score;
+        const int KT = kS1Waves * RPW;
+        const long long wgs = (long long)ceil_div(N, IPW) * nt * ceil_div(K, KT);
+        if (wgs > 0x7fffffffLL) return;
+        const double m = RPW * (double)Cc * R * S * density;
+        const double imb = 1.0 + 1.42 / std::sqrt(std::max(m, 1.0));
+        const double wg_cycles = kS1Waves * RPW * row_nnz * 2.0 * (IPW * PI + 3) * imb +
+                                 nchunks * (1500.0 + IPW * (double)Cc * PLp / 32.0) + (pool ? 1500.0 * RPW : 0.0);
+        const double time = (double)ceil_div((int)std::min<long long>(wgs, 1 << 30), 256) * wg_cycles;
+        if (best_time < 0 || time < best_time * 0.999) {
+            best_time = time;
             best.kind = Kind::kStride1;
             best.PI = PI;
             best.IPW = IPW;
+            best.RPW = RPW;
             best.TH = TH;
             best.ntiles_y = nt;
             best.ipw = IPW;
@@ -657,23 +775,21 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, in
             best.img_lds = Cc * PLp;
             best.buf_floats = ceil_div(IPW * Cc * PLp + slack, 64) * 64;
             best.wv = Wp;
+            best.rows_per_wg = KT;
+            best.nktiles = ceil_div(K, KT);
+            best.total_wgs = (int)wgs;
             size_t floats = 2 * (size_t)best.buf_floats;
-            if (pool) floats = std::max(floats, (size_t)kS1Waves * IPW * cap);
+            if (pool) floats = std::max(floats, (size_t)kS1Waves * IPW * kWave * PI);
             best.lds_bytes = floats * sizeof(float);
         }
     };
-    for (int PI : kPiSingle) consider(PI, 1);
-    for (int IPW : {2, 4})
-        if (IPW <= N)
-            for (int PI : kPiMulti) consider(PI, IPW);
-    if (best_score < 0) return false;
-    const int groups = ceil_div(N, best.IPW) * best.ntiles_y;
-    best.RPW = (groups * ceil_div(K, 2 * kS1Waves) >= 256) ? 2 : 1;
-    best.rows_per_wg = best.RPW * kS1Waves;
-    best.nktiles = ceil_div(K, best.rows_per_wg);
-    const long long wgs = (long long)groups * best.nktiles;
-    if (wgs > 0x7fffffffLL) return false;
-    best.total_wgs = (int)wgs;
+    for (int RPW : {1, 2, 4}) {
+        for (int PI : kPiSingle) consider(PI, 1, RPW);
+        for (int IPW : {2, 4})
+            if (IPW <= N)
+                for (int PI : kPiMulti) consider(PI, IPW, RPW);
+    }
+    if (best_time < 0) return false;
     *out = best;
     return true;
 }
@@ -741,32 +857,10 @@ bool plan_generic(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int strid
     return true;
 }
 
-using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_t *, const float *,
-                           const float *, float *);
-
-template <int PI, int IPW>
-FwdKernel pick_s1_rpw(int RPW, bool pool) {
-    if (RPW == 2) return pool ? spconv_s1_kernel<PI, IPW, 2, true> : spconv_s1_kernel<PI, IPW, 2, false>;
-    return pool ? spconv_s1_kernel<PI, IPW, 1, true> : spconv_s1_kernel<PI, IPW, 1, false>;
-}
-
-template <int IPW, int... PIs>
-FwdKernel pick_s1_pi(int PI, int RPW, bool pool) {
-    FwdKernel k = nullptr;
-    ((PI == PIs ? (k = pick_s1_rpw<PIs, IPW>(RPW, pool), 0) : 0), ...);
-    return k;
-}
-
 FwdKernel pick_kernel(const Plan &pl, bool pool) {
     if (pl.kind == Kind::kGeneric)
         return pool ? spconv_generic_kernel<4, 4, true> : spconv_generic_kernel<4, 4, false>;
-    switch (pl.IPW) {
-        case 1:
-            return pick_s1_pi<1, 32, 30, 28, 26, 24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4>(pl.PI, pl.RPW, pool);
-        case 2: return pick_s1_pi<2, 8, 6, 4, 2>(pl.PI, pl.RPW, pool);
-        case 4: return pick_s1_pi<4, 8, 6, 4, 2>(pl.PI, pl.RPW, pool);
-        default: return nullptr;
-    }
+    return pick_s1(pl.PI, pl.IPW, pl.RPW, pool);
 }
 
 bool out_extent(int in, int f, int stride, int pad, int *o) {
@@ -846,7 +940,7 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     if (pool && (Ho < 2 || Wo < 2)) return SPCONV_EINVAL;
 
     Plan pl;
-    const bool ok = (stride == 1) ? plan_stride1(N, C, K, (int)Hp, (int)Wp, Ho, Wo, R, S, pool, &pl)
+    const bool ok = (stride == 1) ? plan_stride1(N, C, K, (int)Hp, (int)Wp, Ho, Wo, R, S, pool, csr->nnz, &pl)
                                   : plan_generic(N, C, K, (int)Hp, (int)Wp, Ho, Wo, stride, R, pool, &pl);
     if (!ok) return SPCONV_EINVAL;
     FwdArgs a;
