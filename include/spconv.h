@@ -59,6 +59,9 @@ typedef struct spconv_csr {
     const int32_t *colidx; /* [nnz]; not read by spconv_forward (may be NULL there) */
     const int32_t *offset; /* [nnz] */
     const float *vals;     /* [nnz]; the filter values, bit-copied */
+    int64_t max_row_nnz;   /* optional planning hint for spconv_forward: the largest row's entry
+                              count (rowptr[k+1] - rowptr[k]), or 0 if unknown. It only steers the
+                              choice of tiling; results do not depend on it. Must lie in [0, nnz]. */
 } spconv_csr;
 
 /*
@@ -122,7 +125,8 @@ int spconv_pad_input(const float *in, int N, int C, int H, int W, int pad, float
  * Summation order inside one output is unspecified (fp32 arithmetic; results
  * are reproducible run to run for a given device and shape).
  * Errors: SPCONV_EINVAL (NULL pointer, sizes < 1, stride < 1, pad < 0, shape
- * mismatch with csr, nnz outside [0, 2^31), unknown flag bits, empty output,
+ * mismatch with csr, nnz outside [0, 2^31), csr->max_row_nnz outside [0, nnz],
+ * unknown flag bits, empty output,
  * Ho or Wo < 2 with the pool flag, C*Hp*Wp >= 2^31); SPCONV_EHIP when the
  * launch fails.
  */

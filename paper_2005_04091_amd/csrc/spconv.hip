@@ -160,7 +160,7 @@ __device__ __forceinline__ void wait_async_copies() { asm volatile("s_waitcnt vm
 
 // ---- Stride-1 kernel ------------------------------------------------------
 
-constexpr int kS1Waves = 8;
+constexpr int kS1Waves = 16;
 constexpr int kS1Threads = kS1Waves * kWave;
 constexpr int kS1LdsFloats = 40960;  // 160 KiB: one workgroup per CU, two chunk buffers
 constexpr int kStageBlock = 256;     // floats per 16-byte-per-lane LDS DMA instruction
@@ -305,7 +305,7 @@ __device__ __forceinline__ void run_slot(float (&acc)[IPW][PI], int lo, float w,
 }
 
 template <int PI, int IPW, int RPW, bool POOL>
-__global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2))) void spconv_s1_kernel(
+__global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4))) void spconv_s1_kernel(
     FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ offset,
     const float *__restrict__ vals, const float *__restrict__ bias, float *__restrict__ out) {
     extern __shared__ float lds[];
@@ -445,9 +445,10 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2
         }
     } else {
         // Each wave stages its own rows' activated tiles (all images) in LDS,
-        // then reduces 2x2 windows; no other wave touches that area. The last
-        // barrier of the chunk loop ordered these writes after every read of
-        // the input buffers.
+        // then reduces 2x2 windows; no other wave touches that area, so only
+        // the wave's own LDS order matters (its LDS operations execute in
+        // issue order). The last barrier of the chunk loop ordered these
+        // writes after every read of the input buffers by any wave.
         constexpr int kImgPx = kWave * PI;
         float *st = lds + wave * IPW * kImgPx;
         const int prow0 = y0 / 2;
@@ -457,7 +458,6 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2
         for (int i = 0; i < RPW; ++i) {
             const int k = krow[i];
             const float bk = (k < a.K && bias) ? bias[k] : 0.0f;
-            if (i > 0) __syncthreads();
 #pragma unroll
             for (int im = 0; im < IPW; ++im)
 #pragma unroll
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(2, 2
                     if (a.relu) v = v > 0.0f ? v : 0.0f;
                     st[im * kImgPx + lane + kWave * p] = v;
                 }
-            __syncthreads();
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the whole tile is staged
             if (k < a.K) {
                 for (int t = lane; t < IPW * per_img; t += kWave) {
                     const int im = t / per_img;
@@ -669,10 +669,11 @@ using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_
 
 template <int PI, int IPW>
 FwdKernel pick_s1_rpw(int RPW, bool pool) {
-    // Accumulators per lane: RPW * IPW * PI, kept at or below 64.
-    if constexpr (PI * IPW <= 16)
+    // Four waves per SIMD leave 128 VGPRs per lane: RPW * IPW * PI accumulators
+    // plus two pipeline buffers of IPW * PI, kept at or below 96.
+    if constexpr (PI * IPW <= 8)
         if (RPW == 4) return pool ? spconv_s1_kernel<PI, IPW, 4, true> : spconv_s1_kernel<PI, IPW, 4, false>;
-    if constexpr (PI * IPW <= 32)
+    if constexpr (PI * IPW <= 16)
         if (RPW == 2) return pool ? spconv_s1_kernel<PI, IPW, 2, true> : spconv_s1_kernel<PI, IPW, 2, false>;
     if (RPW == 1) return pool ? spconv_s1_kernel<PI, IPW, 1, true> : spconv_s1_kernel<PI, IPW, 1, false>;
     return nullptr;
@@ -703,20 +704,28 @@ FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool) {
 
 // Picks the stride-1 tiling with the smallest modelled run time. The model
 // counts LDS cycles: every nonzero costs a wave IPW*PI LDS reads (2 cycles
-// each, 64 lanes x 4 bytes at 128 bytes per cycle) plus about three reads'
+// each, 64 lanes x 4 bytes at 128 bytes per cycle) plus about one read's
 // worth of issue overhead (weight and offset broadcast, address add, loop
-// control; fitted to measured rates at 7 to 32 pixels per lane), and the 8
-// waves of a workgroup share one LDS. Per chunk, the workgroup waits for its
-// slowest wave: with m nonzeros per wave and chunk (binomial counts), the
-// expected maximum over 8 waves exceeds the mean by about 1.42 * sqrt(m).
-// Each chunk adds a fixed cost (barrier, pipeline refill) and the LDS writes
-// of its copy, halo rows included; the pooled epilogue adds two barriers per
-// channel of a wave. Workgroups run one per CU, in rounds of 256.
+// control), and the 16 waves of a workgroup share one LDS. Each chunk adds a
+// fixed cost (barrier, pipeline refill) and the LDS writes of its copy, halo
+// rows included; the pooled epilogue adds a staging round (LDS writes and
+// the 2x2 reductions) per channel of a wave. Workgroups run one per CU, in
+// rounds of 256.
+// Uneven nonzero counts between the waves of a workgroup cost little while
+// the slowest wave has at most ~1.3x the mean (the others' LDS bandwidth
+// passes to it as they finish). Beyond that the workgroup waits for it: with
+// one channel per wave that happens for skewed filters (max_row_nnz well
+// above the mean); with two or more, heavy and light channels are paired and
+// the pair sums stay close to the mean. One channel per wave also pays ~3%
+// more for the chunk-to-chunk variation of a single row's counts.
+// The constants were fitted to measured run times of 5-7 tilings each of
+// ResNet, VGG (with and without pooling), conv+pool and narrow 256-channel
+// layers, so that the model orders each layer's tilings as measured.
 bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, int S, bool pool, long long nnz,
-                  Plan *out) {
+                  long long max_row_nnz, Plan *out) {
     const int img_pix = Ho * Wp;
     const double row_nnz = std::max(1.0, (double)nnz / K);
-    const double density = std::max(1e-3, (double)nnz / ((double)K * C * R * S));
+    const double skew = max_row_nnz > 0 ? (double)max_row_nnz / row_nnz : 1.0;
     Plan best;
     double best_time = -1.0;
     auto consider = [&](int PI, int IPW, int RPW) {
@@ -753,10 +762,11 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, in
         const int KT = kS1Waves * RPW;
         const long long wgs = (long long)ceil_div(N, IPW) * nt * ceil_div(K, KT);
         if (wgs > 0x7fffffffLL) return;
-        const double m = RPW * (double)Cc * R * S * density;
-        const double imb = 1.0 + 1.42 / std::sqrt(std::max(m, 1.0));
-        const double wg_cycles = kS1Waves * RPW * row_nnz * 2.0 * (IPW * PI + 3) * imb +
-                                 nchunks * (1500.0 + IPW * (double)Cc * PLp / 32.0) + (pool ? 1500.0 * RPW : 0.0);
+        const double pair_skew = 1.0 + (skew - 1.0) / (2.0 * RPW - 1.0);
+        const double imb = std::max(1.0, (RPW == 1 ? skew : pair_skew) / 1.3) * (RPW == 1 ? 1.03 : 1.0);
+        const double compute = kS1Waves * RPW * row_nnz * 2.0 * (IPW * PI + 1.0) * imb;
+        const double wg_cycles =
+            compute + nchunks * (3000.0 + IPW * (double)Cc * PLp / 32.0) + (pool ? 4000.0 * RPW : 0.0);
         const double time = (double)ceil_div((int)std::min<long long>(wgs, 1 << 30), 256) * wg_cycles;
         if (best_time < 0 || time < best_time * 0.999) {
             best_time = time;
@@ -931,6 +941,7 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     const long long Hp = (long long)H + 2LL * pad, Wp = (long long)W + 2LL * pad;
     if (csr->Hp != Hp || csr->Wp != Wp) return SPCONV_EINVAL;
     if (csr->nnz < 0 || csr->nnz >= (1LL << 31)) return SPCONV_EINVAL;
+    if (csr->max_row_nnz < 0 || csr->max_row_nnz > csr->nnz) return SPCONV_EINVAL;
     if (!csr->rowptr || (csr->nnz > 0 && (!csr->offset || !csr->vals))) return SPCONV_EINVAL;
     if ((long long)C * Hp * Wp >= (1LL << 31)) return SPCONV_EINVAL;
     const bool pool = (flags & SPCONV_MAXPOOL2X2) != 0;
@@ -940,7 +951,7 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     if (pool && (Ho < 2 || Wo < 2)) return SPCONV_EINVAL;
 
     Plan pl;
-    const bool ok = (stride == 1) ? plan_stride1(N, C, K, (int)Hp, (int)Wp, Ho, Wo, R, S, pool, csr->nnz, &pl)
+    const bool ok = (stride == 1) ? plan_stride1(N, C, K, (int)Hp, (int)Wp, Ho, Wo, R, S, pool, csr->nnz, csr->max_row_nnz, &pl)
                                   : plan_generic(N, C, K, (int)Hp, (int)Wp, Ho, Wo, stride, R, pool, &pl);
     if (!ok) return SPCONV_EINVAL;
     FwdArgs a;

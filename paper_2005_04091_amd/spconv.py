@@ -32,7 +32,7 @@ class spconv_csr(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int32), ("C", ctypes.c_int32), ("R", ctypes.c_int32), ("S", ctypes.c_int32),
                 ("Hp", ctypes.c_int32), ("Wp", ctypes.c_int32), ("nnz", ctypes.c_int64),
                 ("rowptr", ctypes.c_void_p), ("colidx", ctypes.c_void_p), ("offset", ctypes.c_void_p),
-                ("vals", ctypes.c_void_p)]
+                ("vals", ctypes.c_void_p), ("max_row_nnz", ctypes.c_int64)]
 
 
 _c_int = ctypes.c_int
@@ -140,9 +140,10 @@ class DeviceCSR:
         self.colidx = torch.from_numpy(np.concatenate([host.colidx, np.zeros(1, np.int32)])).to(device)
         self.offset = torch.from_numpy(np.concatenate([host.offset, np.zeros(1, np.int32)])).to(device)
         self.vals = torch.from_numpy(np.concatenate([host.vals, np.zeros(1, np.float32)])).to(device)
+        max_row = int(np.diff(host.rowptr).max()) if host.K > 0 else 0
         self.struct = spconv_csr(host.K, host.C, host.R, host.S, host.Hp, host.Wp, host.nnz,
                                  self.rowptr.data_ptr(), self.colidx.data_ptr(), self.offset.data_ptr(),
-                                 self.vals.data_ptr())
+                                 self.vals.data_ptr(), max_row)
 
 
 def _dev_ptr(t, name):

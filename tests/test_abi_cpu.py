@@ -181,6 +181,8 @@ def test_forward_and_pad_validate_before_any_gpu_work(sp):
     assert fwd(csr=bad_nnz) == E
     null_rows = sp.spconv_csr(4, 3, 3, 3, 10, 12, 5, None, fake, fake, fake)
     assert fwd(csr=null_rows) == E
+    for bad_hint in (-1, 6):        # the largest row cannot have more entries than the filter
+        assert fwd(csr=sp.spconv_csr(4, 3, 3, 3, 10, 12, 5, fake, fake, fake, fake, bad_hint)) == E
     tiny = sp.spconv_csr(4, 3, 3, 3, 3, 3, 5, fake, fake, fake, fake)
     assert fwd(csr=tiny, H=3, W=3, pad=0, flags=sp.SPCONV_MAXPOOL2X2) == E  # 1x1 output cannot be pooled
     assert lib.spconv_pad_input(None, 1, 1, 4, 4, 1, fake, None) == E
