@@ -133,6 +133,36 @@ int spconv_pad_input(const float *in, int N, int C, int H, int W, int pad, float
 int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S,
                    int stride, int pad, const float *bias, uint32_t flags, float *out, hipStream_t stream);
 
+/* Kernel families reported by spconv_plan. */
+#define SPCONV_KERNEL_STRIDE1 1 /* stride 1: channel-chunked LDS staging, lanes own padded-width pixels */
+#define SPCONV_KERNEL_GENERIC 2 /* any stride */
+
+typedef struct spconv_plan_info {
+    int32_t kernel;                /* SPCONV_KERNEL_STRIDE1 or SPCONV_KERNEL_GENERIC */
+    int32_t pixels_per_lane;       /* virtual output pixels per lane per image */
+    int32_t images_per_group;      /* images sharing one workgroup's tile */
+    int32_t channels_per_wave;     /* output channels (CSR rows) per wave; generic kernel: per workgroup */
+    int32_t tile_rows;             /* output rows per spatial tile */
+    int32_t tiles_per_image;       /* spatial tiles per image */
+    int32_t channels_per_chunk;    /* input channels staged in LDS at a time */
+    int32_t chunks;                /* LDS chunks per tile */
+    int32_t workgroups;            /* grid size */
+    int32_t threads_per_workgroup;
+    int64_t lds_bytes;             /* dynamic LDS per workgroup */
+} spconv_plan_info;
+
+/*
+ * spconv_plan - the launch plan spconv_forward would use for these arguments
+ * (host only, queues nothing). Takes the same arguments as spconv_forward
+ * without the buffers and applies the same checks; csr's arrays are not read.
+ * Meant for tests, tools and reports that need to know which kernel variant
+ * and tiling run.
+ * Errors: those of spconv_forward's argument checks; SPCONV_EINVAL for a NULL
+ * info.
+ */
+int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride, int pad,
+                uint32_t flags, spconv_plan_info *info);
+
 /*
  * spconv_output_shape - stored output plane size for the given layer.
  * Writes *Ho, *Wo (pooled sizes when flags has SPCONV_MAXPOOL2X2).

@@ -931,10 +931,13 @@ extern "C" int spconv_pad_input(const float *in, int N, int C, int H, int W, int
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 
-extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R,
-                              int S, int stride, int pad, const float *bias, uint32_t flags, float *out,
-                              hipStream_t stream) {
-    if (!in_padded || !csr || !out) return SPCONV_EINVAL;
+namespace {
+
+// Host-side checks of a forward call (everything but the buffer pointers) and
+// its launch plan. Returns SPCONV_OK or SPCONV_EINVAL.
+int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride, int pad,
+                    uint32_t flags, Plan *plp, FwdArgs *ap) {
+    if (!csr) return SPCONV_EINVAL;
     if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 || pad < 0) return SPCONV_EINVAL;
     if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2)) return SPCONV_EINVAL;
     if (csr->K != K || csr->C != C || csr->R != R || csr->S != S) return SPCONV_EINVAL;
@@ -951,7 +954,8 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     if (pool && (Ho < 2 || Wo < 2)) return SPCONV_EINVAL;
 
     Plan pl;
-    const bool ok = (stride == 1) ? plan_stride1(N, C, K, (int)Hp, (int)Wp, Ho, Wo, R, S, pool, csr->nnz, csr->max_row_nnz, &pl)
+    const bool ok = (stride == 1) ? plan_stride1(N, C, K, (int)Hp, (int)Wp, Ho, Wo, R, S, pool, csr->nnz,
+                                                 csr->max_row_nnz, &pl)
                                   : plan_generic(N, C, K, (int)Hp, (int)Wp, Ho, Wo, stride, R, pool, &pl);
     if (!ok) return SPCONV_EINVAL;
     FwdArgs a;
@@ -985,8 +989,23 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     if (!div_magic((uint32_t)(Hp * Wp), &a.magic, &a.shift)) return SPCONV_EINVAL;
     // Both kernels address a staged channel at its LDS pitch: PLp (stride 1) or PL.
     a.plane_delta = (int)(Hp * Wp) - (pl.kind == Kind::kStride1 ? pl.PLp : pl.PL);
-    FwdKernel kern = pick_kernel(pl, pool);
-    if (!kern) return SPCONV_EINVAL;
+    if (!pick_kernel(pl, pool)) return SPCONV_EINVAL;
+    *plp = pl;
+    *ap = a;
+    return SPCONV_OK;
+}
+
+}  // namespace
+
+extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R,
+                              int S, int stride, int pad, const float *bias, uint32_t flags, float *out,
+                              hipStream_t stream) {
+    if (!in_padded || !out) return SPCONV_EINVAL;
+    Plan pl;
+    FwdArgs a;
+    const int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, &pl, &a);
+    if (rc != SPCONV_OK) return rc;
+    FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0);
     const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
     if (pl.lds_bytes > 65536 &&
         hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds_bytes) !=
@@ -995,4 +1014,26 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
     hipLaunchKernelGGL(kern, dim3((unsigned)pl.total_wgs), dim3(threads), pl.lds_bytes, stream, a, in_padded,
                        csr->rowptr, csr->offset, csr->vals, bias, out);
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
+extern "C" int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride,
+                           int pad, uint32_t flags, spconv_plan_info *info) {
+    if (!info) return SPCONV_EINVAL;
+    Plan pl;
+    FwdArgs a;
+    const int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, &pl, &a);
+    if (rc != SPCONV_OK) return rc;
+    const bool s1 = pl.kind == Kind::kStride1;
+    info->kernel = s1 ? SPCONV_KERNEL_STRIDE1 : SPCONV_KERNEL_GENERIC;
+    info->pixels_per_lane = s1 ? pl.PI : pl.P;
+    info->images_per_group = pl.ipw;
+    info->channels_per_wave = s1 ? pl.RPW : pl.KT;
+    info->tile_rows = pl.TH;
+    info->tiles_per_image = pl.ntiles_y;
+    info->channels_per_chunk = pl.Cc;
+    info->chunks = pl.nchunks;
+    info->workgroups = pl.total_wgs;
+    info->threads_per_workgroup = (int32_t)(s1 ? kS1Threads : kThreads);
+    info->lds_bytes = (int64_t)pl.lds_bytes;
+    return SPCONV_OK;
 }

@@ -24,7 +24,10 @@ SPCONV_EHIP = -3
 SPCONV_RELU = 1
 SPCONV_MAXPOOL2X2 = 2
 
-EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_output_shape", "spconv_strerror")
+EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_plan", "spconv_output_shape",
+            "spconv_strerror")
+SPCONV_KERNEL_STRIDE1 = 1
+SPCONV_KERNEL_GENERIC = 2
 
 
 class spconv_csr(ctypes.Structure):
@@ -33,6 +36,15 @@ class spconv_csr(ctypes.Structure):
                 ("Hp", ctypes.c_int32), ("Wp", ctypes.c_int32), ("nnz", ctypes.c_int64),
                 ("rowptr", ctypes.c_void_p), ("colidx", ctypes.c_void_p), ("offset", ctypes.c_void_p),
                 ("vals", ctypes.c_void_p), ("max_row_nnz", ctypes.c_int64)]
+
+
+class spconv_plan_info(ctypes.Structure):
+    """Mirror of ``struct spconv_plan_info``."""
+    _fields_ = [("kernel", ctypes.c_int32), ("pixels_per_lane", ctypes.c_int32), ("images_per_group", ctypes.c_int32),
+                ("channels_per_wave", ctypes.c_int32), ("tile_rows", ctypes.c_int32),
+                ("tiles_per_image", ctypes.c_int32), ("channels_per_chunk", ctypes.c_int32),
+                ("chunks", ctypes.c_int32), ("workgroups", ctypes.c_int32), ("threads_per_workgroup", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int64)]
 
 
 _c_int = ctypes.c_int
@@ -49,6 +61,9 @@ def _bind(lib):
     lib.spconv_forward.restype = _c_int
     lib.spconv_forward.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int,
                                    _c_int, _c_int, _c_int, _vp, ctypes.c_uint32, _vp, _vp]
+    lib.spconv_plan.restype = _c_int
+    lib.spconv_plan.argtypes = [_c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int, _c_int,
+                                _c_int, _c_int, ctypes.c_uint32, ctypes.POINTER(spconv_plan_info)]
     lib.spconv_output_shape.restype = _c_int
     lib.spconv_output_shape.argtypes = [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_uint32,
                                         ctypes.POINTER(_c_int), ctypes.POINTER(_c_int)]
@@ -189,6 +204,16 @@ def spconv_forward(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R
     return out
 
 
+def spconv_plan(N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int, pad: int,
+                flags: int = SPCONV_RELU) -> dict:
+    """The launch plan ``spconv_forward`` would use, as a dict of the
+    ``spconv_plan_info`` fields."""
+    info = spconv_plan_info()
+    _check(_lib.spconv_plan(N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad, flags, ctypes.byref(info)),
+           "spconv_plan")
+    return {name: getattr(info, name) for name, _ in spconv_plan_info._fields_}
+
+
 def flags_of(relu: bool, pool: bool) -> int:
     return (SPCONV_RELU if relu else 0) | (SPCONV_MAXPOOL2X2 if pool else 0)
 
@@ -218,6 +243,10 @@ class SparseConvLayer:
         N = int(xp.shape[0])
         return spconv_forward(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
                               self.pad, self.bias, self.flags, out=out, stream=stream)
+
+    def plan(self, N: int) -> dict:
+        return spconv_plan(N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride, self.pad,
+                           self.flags)
 
     def run(self, x, xp=None, out=None, stream=None):
         xp = self.pad_input(x, out=xp, stream=stream)

@@ -34,7 +34,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(
-        ["spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_output_shape", "spconv_strerror"])
+        ["spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_plan", "spconv_output_shape",
+         "spconv_strerror"])
 
 
 def test_library_exports_every_declared_symbol(sp):
@@ -189,3 +190,37 @@ def test_forward_and_pad_validate_before_any_gpu_work(sp):
     assert lib.spconv_pad_input(fake, 1, 1, 0, 4, 1, fake, None) == E
     assert lib.spconv_pad_input(fake, 1, 1, 4, 4, -1, fake, None) == E
     assert lib.spconv_pad_input(fake, 1, 1, 4, 4, 1, None, None) == E
+
+
+def test_plan_reports_the_launch_without_a_gpu(sp):
+    """spconv_plan runs the forward call's host checks and planner only; fake
+    (never dereferenced) addresses stand in for the CSR arrays."""
+    lib = sp._lib
+    fake = 0x1000
+
+    def plan(N, C, H, W, K, R=3, S=3, stride=1, pad=1, flags=sp.SPCONV_RELU, nnz=None, max_row=0):
+        nnz = int(0.2 * K * C * R * S) if nnz is None else nnz
+        csr = sp.spconv_csr(K, C, R, S, H + 2 * pad, W + 2 * pad, nnz, fake, fake, fake, fake, max_row)
+        info = sp.spconv_plan_info()
+        rc = lib.spconv_plan(N, C, H, W, ctypes.byref(csr), K, R, S, stride, pad, flags, ctypes.byref(info))
+        return rc, info
+
+    rc, p = plan(32, 64, 56, 56, 64)                      # ResNet-style layer
+    assert rc == sp.SPCONV_OK
+    assert p.kernel == sp.SPCONV_KERNEL_STRIDE1 and p.threads_per_workgroup == 1024
+    # the grid covers every (image group, spatial tile, channel tile) exactly once
+    kt = 16 * p.channels_per_wave
+    assert p.workgroups == -(-32 // p.images_per_group) * p.tiles_per_image * -(-64 // kt)
+    assert p.tile_rows * p.tiles_per_image >= 56 and p.tile_rows * (p.tiles_per_image - 1) < 56
+    assert p.channels_per_chunk * p.chunks >= 64 and p.channels_per_chunk * (p.chunks - 1) < 64
+    assert 0 < p.lds_bytes <= 160 * 1024
+    # a filter with a dense channel makes the planner pair channels per wave
+    rc, flat = plan(32, 256, 14, 14, 256, nnz=117965, max_row=117965 // 256)
+    rc2, skewed = plan(32, 256, 14, 14, 256, nnz=117965, max_row=3 * 117965 // 256)
+    assert rc == rc2 == sp.SPCONV_OK and skewed.channels_per_wave >= 2
+    rc, p = plan(2, 5, 9, 8, 7, stride=2)                   # strided layers take the any-stride kernel
+    assert rc == sp.SPCONV_OK and p.kernel == sp.SPCONV_KERNEL_GENERIC
+    assert plan(2, 5, 9, 8, 7, max_row=10 ** 9)[0] == sp.SPCONV_EINVAL  # hint above nnz
+    assert plan(2, 5, 9, 8, 7, flags=8)[0] == sp.SPCONV_EINVAL
+    csr = sp.spconv_csr(7, 5, 3, 3, 11, 10, 60, fake, fake, fake, fake, 0)
+    assert lib.spconv_plan(2, 5, 9, 8, ctypes.byref(csr), 7, 3, 3, 1, 1, 1, None) == sp.SPCONV_EINVAL

@@ -230,6 +230,71 @@ def test_vgg_block_chain_full_size(sp):
 
 
 # ---------------------------------------------------------------------------
+# Every stride-1 kernel variant the planner picks: pixels per lane x images
+# per workgroup x channels per wave, pooled or not, one or several LDS chunks,
+# CSR rows with more than a window (128 entries) in one chunk, channel tiles
+# and image groups cut short at the end. The planner's pick is asserted, so a
+# change of the planner that leaves a variant untested fails here.
+# ---------------------------------------------------------------------------
+
+VARIANTS = [
+    # name, N, C, K, H(=W), pool, skewed rows, expected (PI, IPW, RPW)
+    ("ipw1_rpw2", 8, 3, 520, 12, False, True, (4, 1, 2)),
+    ("ipw1_rpw2_pool", 8, 8, 520, 12, True, True, (4, 1, 2)),
+    ("ipw1_rpw4", 16, 3, 520, 12, False, True, (4, 1, 4)),
+    ("ipw2_rpw1", 8, 3, 520, 2, False, False, (2, 2, 1)),
+    ("ipw2_rpw1_pool", 8, 3, 520, 2, True, False, (2, 2, 1)),
+    ("ipw2_rpw2", 16, 3, 520, 2, False, True, (2, 2, 2)),
+    ("ipw2_rpw2_pool", 16, 8, 520, 2, True, True, (2, 2, 2)),
+    ("ipw2_rpw4", 32, 3, 520, 2, False, True, (2, 2, 4)),
+    ("ipw4_rpw2_ragged_n", 31, 3, 520, 2, False, False, (2, 4, 2)),
+    ("ipw4_rpw4", 64, 3, 520, 2, False, False, (2, 4, 4)),
+    ("ipw4_rpw4_pool", 64, 3, 520, 2, True, False, (2, 4, 4)),
+    ("ipw2_rpw2_chunks_overflow", 16, 200, 520, 2, False, True, (2, 2, 2)),
+    ("ipw2_rpw1_chunks", 32, 200, 520, 2, False, False, (2, 2, 1)),
+    ("ipw1_rpw4_chunks_overflow", 16, 100, 520, 12, False, True, (4, 1, 4)),
+    ("ipw1_rpw2_pool_chunks_overflow", 8, 100, 520, 12, True, True, (4, 1, 2)),
+]
+
+
+@pytest.mark.parametrize("case", VARIANTS, ids=[v[0] for v in VARIANTS])
+def test_kernel_variant(sp, case):
+    import torch
+    name, N, C, K, H, pool, skew, expect = case
+    layer = synth.random_layer(4242, N, C, K, H, H, density=0.3, pool=pool, skew=skew)
+    L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, H, 1, 1, True, pool)
+    plan = L.plan(N)
+    say("variant", name, layer.shape, plan)
+    assert (plan["pixels_per_lane"], plan["images_per_group"], plan["channels_per_wave"]) == expect
+    out = L.run(torch.from_numpy(layer.x).cuda())
+    torch.cuda.synchronize()
+    ref, ab = oracle_layer(layer)
+    check_close(out.cpu().numpy(), ref, ab, name)
+
+
+def test_plan_hint_changes_tiling_not_results(sp):
+    """Without the max_row_nnz hint the planner takes another tiling for a
+    skewed filter; every output still sums its row's entries in CSR order, so
+    both runs agree bit for bit (and with the oracle)."""
+    import torch
+    layer = synth.random_layer(4343, 32, 16, 256, 14, 14, density=0.3, skew=True)
+    N, C, H, W, K, R, S = layer.shape
+    L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, 1, 1, True, False)
+    x = torch.from_numpy(layer.x).cuda()
+    hinted = L.plan(N)
+    a = L.run(x).cpu().numpy()
+    L.csr.struct.max_row_nnz = 0
+    blind = L.plan(N)
+    say("hint", hinted, blind)
+    b = L.run(x).cpu().numpy()
+    assert hinted["channels_per_wave"] != blind["channels_per_wave"] or \
+        hinted["pixels_per_lane"] != blind["pixels_per_lane"]
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    ref, ab = oracle_layer(layer)
+    check_close(a, ref, ab, "hinted")
+
+
+# ---------------------------------------------------------------------------
 # Robustness
 # ---------------------------------------------------------------------------
 
