@@ -55,36 +55,73 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shi
 // Padded input (spconv_pad_input)
 // ---------------------------------------------------------------------------
 
-// One workgroup covers 4*256 consecutive elements of one padded plane; each of
-// its four store instructions writes 256 consecutive floats.
-constexpr int kPadPerThread = 4;
-constexpr int kPadPerBlock = kThreads * kPadPerThread;
+// The padded tensor is treated as one flat array of 4-element quads. A
+// workgroup covers kPadQuads consecutive quads per thread: in round j thread t
+// writes quad (block*kPadQuads + j)*256 + t with one 16-byte store (when the
+// output is 16-byte aligned), so each round's stores coalesce; a quad inside
+// one input row is fetched with one 16-byte load, border quads element by
+// element (0 outside the input). All loads of a thread are issued before its
+// stores.
+constexpr int kPadQuads = 4;
 
 struct PadArgs {
     const float *in;
     float *out;
+    long long total;      // N*C*Hp*Wp
     int H, W, pad, Hp, Wp;
     int plane;            // Hp*Wp
-    int blocks_per_plane;
     uint32_t wp_magic;    // x / Wp == (x * wp_magic) >> wp_shift for 0 <= x < 2^31
     int wp_shift;
 };
 
-__global__ __launch_bounds__(kThreads) void pad_nchw_kernel(PadArgs a) {
-    const uint32_t plane_id = blockIdx.x / (uint32_t)a.blocks_per_plane;
-    const uint32_t blk = blockIdx.x - plane_id * (uint32_t)a.blocks_per_plane;
-    const float *src = a.in + (size_t)plane_id * (size_t)a.H * (size_t)a.W;
-    float *dst = a.out + (size_t)plane_id * (size_t)a.plane;
+__device__ __forceinline__ float4 pad_quad(const PadArgs &a, long long f0) {
+    long long pid = f0 / a.plane;  // plane (n, c) of the first element
+    const int e = (int)(f0 - pid * a.plane);
+    int yp = (int)fast_div((uint32_t)e, a.wp_magic, a.wp_shift);
+    int xp = e - yp * a.Wp;
+    const int y0 = yp - a.pad, x0 = xp - a.pad;
+    if (f0 + 3 < a.total && y0 >= 0 && y0 < a.H && x0 >= 0 && x0 + 3 < a.W) {
+        float4 q;  // all four inside one input row: one 16-byte load (4-byte aligned)
+        __builtin_memcpy(&q, a.in + pid * a.H * a.W + (long long)y0 * a.W + x0, sizeof(q));
+        return q;
+    }
+    float v[4];
 #pragma unroll
-    for (int u = 0; u < kPadPerThread; ++u) {
-        const int e = (int)blk * kPadPerBlock + u * kThreads + (int)threadIdx.x;
-        if (e < a.plane) {
-            const int yp = (int)fast_div((uint32_t)e, a.wp_magic, a.wp_shift);
-            const int xp = e - yp * a.Wp;
-            const int y = yp - a.pad, x = xp - a.pad;
-            float v = 0.0f;
-            if (y >= 0 && y < a.H && x >= 0 && x < a.W) v = src[(size_t)y * a.W + x];
-            dst[e] = v;
+    for (int j = 0; j < 4; ++j) {
+        const int y = yp - a.pad, x = xp - a.pad;
+        v[j] = 0.0f;
+        if (f0 + j < a.total && y >= 0 && y < a.H && x >= 0 && x < a.W)
+            v[j] = a.in[pid * a.H * a.W + (long long)y * a.W + x];
+        if (++xp == a.Wp) {  // next element of the flat array
+            xp = 0;
+            if (++yp == a.Hp) {
+                yp = 0;
+                ++pid;
+            }
+        }
+    }
+    return make_float4(v[0], v[1], v[2], v[3]);
+}
+
+template <bool VEC>
+__global__ __launch_bounds__(kThreads) void pad_nchw_kernel(PadArgs a) {
+    float4 q[kPadQuads];
+    long long f[kPadQuads];
+#pragma unroll
+    for (int j = 0; j < kPadQuads; ++j) {
+        f[j] = (((long long)blockIdx.x * kPadQuads + j) * kThreads + threadIdx.x) * 4;
+        if (f[j] < a.total) q[j] = pad_quad(a, f[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < kPadQuads; ++j) {
+        if (f[j] >= a.total) break;
+        if (VEC && f[j] + 3 < a.total) {
+            *reinterpret_cast<float4 *>(a.out + f[j]) = q[j];
+        } else {
+            const float v[4] = {q[j].x, q[j].y, q[j].z, q[j].w};
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (f[j] + u < a.total) a.out[f[j] + u] = v[u];
         }
     }
 }
@@ -917,17 +954,20 @@ extern "C" int spconv_pad_input(const float *in, int N, int C, int H, int W, int
     PadArgs a;
     a.in = in;
     a.out = out_padded;
+    a.total = planes * plane;
     a.H = H;
     a.W = W;
     a.pad = pad;
     a.Hp = (int)Hp;
     a.Wp = (int)Wp;
     a.plane = (int)plane;
-    a.blocks_per_plane = (int)((plane + kPadPerBlock - 1) / kPadPerBlock);
     if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift)) return SPCONV_EINVAL;
-    const long long blocks = planes * a.blocks_per_plane;
+    const long long per_block = 4LL * kThreads * kPadQuads;
+    const long long blocks = (a.total + per_block - 1) / per_block;
     if (blocks > 0x7fffffffLL) return SPCONV_EINVAL;
-    hipLaunchKernelGGL(pad_nchw_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, a);
+    const bool vec = (reinterpret_cast<uintptr_t>(out_padded) & 15) == 0;
+    hipLaunchKernelGGL(vec ? pad_nchw_kernel<true> : pad_nchw_kernel<false>, dim3((unsigned)blocks), dim3(kThreads),
+                       0, stream, a);
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 

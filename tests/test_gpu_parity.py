@@ -76,6 +76,22 @@ def test_pad_bit_exact(sp, shape, pad):
     assert np.array_equal(xp.cpu().numpy().view(np.uint32), ref.view(np.uint32))
 
 
+def test_pad_unaligned_output_and_guards(sp):
+    """An output that starts 4 bytes past a 16-byte boundary (the kernel's
+    scalar-store variant), between NaN guard words that must survive."""
+    import torch
+    x = np.random.default_rng(8).uniform(-1, 1, (3, 2, 11, 13)).astype(np.float32)
+    ref = oracle.pad(x, 2)
+    buf = torch.full((ref.size + 9,), float("nan"), dtype=torch.float32, device="cuda")
+    out = buf[1:1 + ref.size].view(ref.shape)
+    say("pad unaligned")
+    sp.spconv_pad_input(torch.from_numpy(x).cuda(), 2, out=out)
+    torch.cuda.synchronize()
+    b = buf.cpu().numpy()
+    assert np.isnan(b[0]) and np.isnan(b[1 + ref.size:]).all()
+    assert np.array_equal(b[1:1 + ref.size].view(np.uint32), ref.reshape(-1).view(np.uint32))
+
+
 # ---------------------------------------------------------------------------
 # Forward: small shapes spanning tiles, ragged tails and the degenerate cases
 # ---------------------------------------------------------------------------
