@@ -264,11 +264,16 @@ __device__ __forceinline__ RawWindow fetch_window(const int32_t *__restrict__ of
     return r;
 }
 
-// A window decoded for one channel chunk: LDS float indices of its entries and
-// the number n of them that belong to the chunk (a prefix of the window).
+// A window decoded for one channel chunk: per slot, the LDS float index of
+// each entry's tap for virtual pixel 0 rounded down to even (`lo`), its
+// weight, and two lane masks that split the entries of the chunk (a prefix of
+// the window) by the parity of that index; `n` counts them. Even taps are read
+// as aligned pixel pairs (2l, 2l+1); odd taps as the aligned pairs (2l-1, 2l),
+// which accumulate into the pixel-shifted accumulator set.
 struct Window {
     int lo[2];
     float w[2];
+    uint64_t even[2], odd[2];
     int n;
 };
 
@@ -281,32 +286,51 @@ __device__ __forceinline__ Window decode_window(const FwdArgs &a, const RawWindo
         const int o = r.o[h];
         const bool in = r.base + h * kWave + lane < e && o < bound;
         const int c = (int)fast_div((uint32_t)o, a.magic, a.shift);
-        win.lo[h] = vb + o - c * a.plane_delta;
+        const int t = vb + o - c * a.plane_delta;
+        const int odd = t & 1;
+        win.lo[h] = t - odd;
         // Touch the loaded weight here, so that the wait for its load is
         // placed at this decode and not deferred into the compute loop, where
         // it would also wait for the chunk copies in flight.
         float w = r.w[h];
         asm volatile("" : "+v"(w));
         win.w[h] = w;
-        win.n += __builtin_popcountll(__builtin_amdgcn_ballot_w64(in));
+        win.even[h] = __builtin_amdgcn_ballot_w64(in && !odd);
+        win.odd[h] = __builtin_amdgcn_ballot_w64(in && odd);
+        win.n += __builtin_popcountll(win.even[h] | win.odd[h]);
     }
     return win;
 }
 
-template <int PI, int IPW>
-__device__ __forceinline__ void load_taps(float (&x)[IPW][PI], const float *lds, int ad, int img_lds) {
+// Pixel pairs of one tap: x[im][j] = the two floats at LDS index ad + 128*j of
+// image block im (ad even, so every read is one aligned ds_read_b64).
+// The loads are volatile LDS accesses of a clang vector type:
+//  * volatile keeps the compiler from fusing two of them into one
+//    ds_read2st64_b64, which gfx950 serves at half the bandwidth of two
+//    ds_read_b64 (about 127 vs 230-250 bytes per clock per CU);
+//  * a vector type rather than HIP's float2 struct, because through the
+//    struct the compiler also waits for the chunk copies in flight before
+//    each read.
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef const volatile __attribute__((address_space(3))) f32x2 lds_pair_t;
+
+template <int PJ, int IPW>
+__device__ __forceinline__ void load_pairs(f32x2 (&x)[IPW][PJ], const float *lds, int ad, int img_lds) {
 #pragma unroll
     for (int im = 0; im < IPW; ++im)
 #pragma unroll
-        for (int p = 0; p < PI; ++p) x[im][p] = lds[ad + im * img_lds + kWave * p];
+        for (int p = 0; p < PJ; ++p) x[im][p] = *(lds_pair_t *)(lds + ad + im * img_lds + 2 * kWave * p);
 }
 
-template <int PI, int IPW>
-__device__ __forceinline__ void fma_taps(float (&acc)[IPW][PI], const float (&x)[IPW][PI], float v) {
+template <int PJ, int IPW>
+__device__ __forceinline__ void fma_pairs(float2 (&acc)[IPW][PJ], const f32x2 (&x)[IPW][PJ], float v) {
 #pragma unroll
     for (int im = 0; im < IPW; ++im)
 #pragma unroll
-        for (int p = 0; p < PI; ++p) acc[im][p] = fmaf(v, x[im][p], acc[im][p]);
+        for (int p = 0; p < PJ; ++p) {
+            acc[im][p].x = fmaf(v, x[im][p].x, acc[im][p].x);
+            acc[im][p].y = fmaf(v, x[im][p].y, acc[im][p].y);
+        }
 }
 
 __device__ __forceinline__ int lane_read_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
@@ -314,30 +338,66 @@ __device__ __forceinline__ float lane_read_f(float v, int l) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
-// Accumulate entries [0, n) of one window slot (n <= 64) into acc. Two-stage
-// software pipeline: the LDS reads of entry u+1 are in flight while the FMAs of
-// entry u issue. The loop body is branch-free so the accumulators and both
-// buffers keep their registers: past the last entry it re-reads that entry and
-// adds it with weight 0 (exact for finite inputs).
-template <int PI, int IPW>
-__device__ __forceinline__ void run_slot(float (&acc)[IPW][PI], int lo, float w, int n, const float *lds, int q,
-                                         int img_lds) {
-    if (n <= 0) return;
-    float x0[IPW][PI], x1[IPW][PI];
-    load_taps(x0, lds, lane_read_i(lo, 0) + q, img_lds);
+// Accumulate the window entries whose lanes are set in mask m into acc. Two-
+// stage software pipeline: the LDS reads of the next entry are in flight
+// while the FMAs of the current one issue; the entries are visited in lane
+// order through the mask's set bits (scalar find-first-set). The loop body
+// has no exit in the middle, so the accumulators stay in place.
+template <int PJ, int IPW>
+__device__ __forceinline__ void run_mask(float2 (&acc)[IPW][PJ], int lo, float w, uint64_t m, const float *lds,
+                                         int q, int img_lds) {
+    int n = __builtin_popcountll(m);
+    if (n == 0) return;
+    f32x2 x0[IPW][PJ], x1[IPW][PJ];
+    int u0 = __builtin_ctzll(m);
+    m &= m - 1;
+    load_pairs(x0, lds, lane_read_i(lo, u0) + q, img_lds);
+    float w0 = lane_read_f(w, u0);
     // The scheduling barriers keep each refill after the FMAs that read the
     // buffer it overwrites, so the two buffers alternate without copies.
-    for (int u = 0; u < n; u += 2) {
-        const int u1 = min(u + 1, n - 1), u2 = min(u + 2, n - 1);
-        const float w0 = lane_read_f(w, u);
-        const int w1_bits = lane_read_i(__float_as_int(w), u1);
-        const float w1 = __int_as_float((u + 1 < n) ? w1_bits : 0);
-        load_taps(x1, lds, lane_read_i(lo, u1) + q, img_lds);
-        fma_taps(acc, x0, w0);
+    for (; n > 2; n -= 2) {
+        const int u1 = __builtin_ctzll(m);
+        m &= m - 1;
+        const float w1 = lane_read_f(w, u1);
+        load_pairs(x1, lds, lane_read_i(lo, u1) + q, img_lds);
+        fma_pairs(acc, x0, w0);
         __builtin_amdgcn_sched_barrier(0);
-        load_taps(x0, lds, lane_read_i(lo, u2) + q, img_lds);
-        fma_taps(acc, x1, w1);
+        u0 = __builtin_ctzll(m);
+        m &= m - 1;
+        w0 = lane_read_f(w, u0);
+        load_pairs(x0, lds, lane_read_i(lo, u0) + q, img_lds);
+        fma_pairs(acc, x1, w1);
         __builtin_amdgcn_sched_barrier(0);
+    }
+    if (n == 2) {
+        const int u1 = __builtin_ctzll(m);
+        const float w1 = lane_read_f(w, u1);
+        load_pairs(x1, lds, lane_read_i(lo, u1) + q, img_lds);
+        fma_pairs(acc, x0, w0);
+        __builtin_amdgcn_sched_barrier(0);
+        fma_pairs(acc, x1, w1);
+    } else {
+        fma_pairs(acc, x0, w0);
+    }
+}
+
+// Sums of this lane's virtual pixel pairs (2l + 128j, 2l+1 + 128j) of one
+// image: the even-tap pairs plus the odd-tap pairs, which are shifted by one
+// pixel (lane l holds pixels 2l-1 and 2l). Pixel 2l+1 takes the odd pair of
+// lane l+1; lane 63 takes lane 0 of pair j+1. The last virtual pixel of the
+// tile (lane 63, last pair) has no such source: the planner keeps every tile
+// below 64*PI pixels, so that pixel is never stored.
+template <int PJ>
+__device__ __forceinline__ void merge_pairs(const float2 (&e)[PJ], const float2 (&o)[PJ], float2 (&v)[PJ], int lane) {
+    const int src = ((lane + 1) & (kWave - 1)) * 4;
+    float rot[PJ];
+#pragma unroll
+    for (int p = 0; p < PJ; ++p) rot[p] = __int_as_float(__builtin_amdgcn_ds_bpermute(src, __float_as_int(o[p].x)));
+#pragma unroll
+    for (int p = 0; p < PJ; ++p) {
+        const float next = p + 1 < PJ ? rot[p + 1] : 0.0f;
+        const float right = lane == kWave - 1 ? next : rot[p];
+        v[p] = make_float2(e[p].x + o[p].y, e[p].y + right);
     }
 }
 
@@ -347,6 +407,8 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
     const float *__restrict__ vals, const float *__restrict__ bias, float *__restrict__ out) {
     extern __shared__ float lds[];
     constexpr int KT = RPW * kS1Waves;  // output channels per workgroup
+    constexpr int PJ = PI / 2;          // pixel pairs per lane per image
+    static_assert(PI % 2 == 0, "pixels per lane come in pairs");
 
     const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
@@ -360,8 +422,8 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 
     // Output channels of this wave. With RPW > 1 the workgroup's KT channels
     // are ranked by nonzero count and dealt to the waves in snake order (ranks
-    // w, 2*8-1-w, 2*8+w, ...), so heavy and light channels share a wave and the
-    // waves' loads even out.
+    // w, 2*16-1-w, 2*16+w, ...), so heavy and light channels share a wave and
+    // the waves' loads even out.
     int krow[RPW];
     if constexpr (RPW == 1) {
         krow[0] = kt * KT + wave;
@@ -389,17 +451,23 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
         end[i] = (k < a.K) ? rowptr[k + 1] : 0;
     }
 
-    float acc[RPW][IPW][PI];
+    // accE: pixels (2l + 128j, 2l+1 + 128j) from even taps; accO: pixels
+    // (2l-1 + 128j, 2l + 128j) from odd taps.
+    float2 accE[RPW][IPW][PJ], accO[RPW][IPW][PJ];
 #pragma unroll
     for (int i = 0; i < RPW; ++i)
 #pragma unroll
         for (int im = 0; im < IPW; ++im)
 #pragma unroll
-            for (int p = 0; p < PI; ++p) acc[i][im][p] = 0.0f;
+            for (int p = 0; p < PJ; ++p) {
+                accE[i][im][p] = make_float2(0.0f, 0.0f);
+                accO[i][im][p] = make_float2(0.0f, 0.0f);
+            }
 
     // LDS float index of tap offset o for chunk ch, pixel q: vb(ch) + o - c*plane_delta + q.
     auto vb_of = [&](int ch) { return (ch & 1) * a.buf_floats - ch * a.Cc * a.PLp; };
     auto bound_of = [&](int ch) { return min((ch + 1) * a.Cc, a.C) * plane; };
+    const int q = 2 * lane;
 
     Window win[RPW];
     RawWindow next[RPW];
@@ -426,9 +494,12 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             for (;;) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    run_mask(accE[i], win[i].lo[h], win[i].w[h], win[i].even[h], lds, q, a.img_lds);
+                    run_mask(accO[i], win[i].lo[h], win[i].w[h], win[i].odd[h], lds, q, a.img_lds);
+                }
                 const int n = win[i].n;
-                run_slot(acc[i], win[i].lo[0], win[i].w[0], min(n, kWave), lds, lane, a.img_lds);
-                run_slot(acc[i], win[i].lo[1], win[i].w[1], n - kWave, lds, lane, a.img_lds);
                 cur[i] += n;
                 if (n < 2 * kWave || cur[i] >= end[i]) break;
                 // The row has more entries in this chunk than one window holds.
@@ -454,14 +525,16 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 
     const int tile_px = a.TH * a.Wp;
     if constexpr (!POOL) {
-        int pix[PI];  // in-plane output index of each of this lane's pixels, or -1
+        int pix[PJ][2];  // in-plane output index of each of this lane's pixels, or -1
 #pragma unroll
-        for (int p = 0; p < PI; ++p) {
-            const int q = lane + kWave * p;
-            const int yl = q / a.Wp, x = q - yl * a.Wp;
-            const int y = y0 + yl;
-            pix[p] = (q < tile_px && x < a.Wo && y < a.Ho) ? y * a.Wo + x : -1;
-        }
+        for (int p = 0; p < PJ; ++p)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int qq = q + 2 * kWave * p + h;
+                const int yl = qq / a.Wp, x = qq - yl * a.Wp;
+                const int y = y0 + yl;
+                pix[p][h] = (qq < tile_px && x < a.Wo && y < a.Ho) ? y * a.Wo + x : -1;
+            }
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             const int k = krow[i];
@@ -472,11 +545,17 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
                 const int n = ig * IPW + im;
                 if (n >= a.N) break;
                 float *op = out + ((size_t)n * a.K + k) * (size_t)a.Ho * a.Wo;
+                float2 sum[PJ];
+                merge_pairs(accE[i][im], accO[i][im], sum, lane);
 #pragma unroll
-                for (int p = 0; p < PI; ++p) {
-                    float v = acc[i][im][p] + bk;
-                    if (a.relu) v = v > 0.0f ? v : 0.0f;
-                    if (pix[p] >= 0) op[pix[p]] = v;
+                for (int p = 0; p < PJ; ++p) {
+                    float v0 = sum[p].x + bk, v1 = sum[p].y + bk;
+                    if (a.relu) {
+                        v0 = v0 > 0.0f ? v0 : 0.0f;
+                        v1 = v1 > 0.0f ? v1 : 0.0f;
+                    }
+                    if (pix[p][0] >= 0) op[pix[p][0]] = v0;
+                    if (pix[p][1] >= 0) op[pix[p][1]] = v1;
                 }
             }
         }
@@ -496,13 +575,19 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
             const int k = krow[i];
             const float bk = (k < a.K && bias) ? bias[k] : 0.0f;
 #pragma unroll
-            for (int im = 0; im < IPW; ++im)
+            for (int im = 0; im < IPW; ++im) {
+                float2 sum[PJ];
+                merge_pairs(accE[i][im], accO[i][im], sum, lane);
 #pragma unroll
-                for (int p = 0; p < PI; ++p) {
-                    float v = acc[i][im][p] + bk;
-                    if (a.relu) v = v > 0.0f ? v : 0.0f;
-                    st[im * kImgPx + lane + kWave * p] = v;
+                for (int p = 0; p < PJ; ++p) {
+                    float v0 = sum[p].x + bk, v1 = sum[p].y + bk;
+                    if (a.relu) {
+                        v0 = v0 > 0.0f ? v0 : 0.0f;
+                        v1 = v1 > 0.0f ? v1 : 0.0f;
+                    }
+                    *reinterpret_cast<float2 *>(st + im * kImgPx + q + 2 * kWave * p) = make_float2(v0, v1);
                 }
+            }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the whole tile is staged
             if (k < a.K) {
                 for (int t = lane; t < IPW * per_img; t += kWave) {
@@ -706,13 +791,15 @@ using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_
 
 template <int PI, int IPW>
 FwdKernel pick_s1_rpw(int RPW, bool pool) {
-    // Four waves per SIMD leave 128 VGPRs per lane: RPW * IPW * PI accumulators
-    // plus two pipeline buffers of IPW * PI, kept at or below 96.
+    // Four waves per SIMD leave 128 VGPRs per lane: two accumulator sets of
+    // RPW * IPW * PI (even and odd taps) plus two pipeline buffers of IPW * PI,
+    // kept at or below 96, the largest tilings that compile without spills.
     if constexpr (PI * IPW <= 8)
         if (RPW == 4) return pool ? spconv_s1_kernel<PI, IPW, 4, true> : spconv_s1_kernel<PI, IPW, 4, false>;
     if constexpr (PI * IPW <= 16)
         if (RPW == 2) return pool ? spconv_s1_kernel<PI, IPW, 2, true> : spconv_s1_kernel<PI, IPW, 2, false>;
-    if (RPW == 1) return pool ? spconv_s1_kernel<PI, IPW, 1, true> : spconv_s1_kernel<PI, IPW, 1, false>;
+    if constexpr (PI * IPW <= 24)
+        if (RPW == 1) return pool ? spconv_s1_kernel<PI, IPW, 1, true> : spconv_s1_kernel<PI, IPW, 1, false>;
     return nullptr;
 }
 
@@ -725,14 +812,13 @@ FwdKernel pick_s1_pi(int PI, int RPW, bool pool) {
 
 // Pixels per lane per image (PI), images per wave (IPW) and channels per wave
 // (RPW) the stride-1 kernel is built for.
-constexpr int kPiSingle[] = {32, 30, 28, 26, 24, 22, 20, 18, 16, 14, 13, 12, 11, 10, 9, 8, 7, 6, 5, 4};
+constexpr int kPiSingle[] = {24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4};
 constexpr int kPiMulti[] = {8, 6, 4, 2};
 
 FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool) {
     switch (IPW) {
         case 1:
-            return pick_s1_pi<1, 32, 30, 28, 26, 24, 22, 20, 18, 16, 14, 13, 12, 11, 10, 9, 8, 7, 6, 5, 4>(PI, RPW,
-                                                                                                          pool);
+            return pick_s1_pi<1, 24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4>(PI, RPW, pool);
         case 2: return pick_s1_pi<2, 8, 6, 4, 2>(PI, RPW, pool);
         case 4: return pick_s1_pi<4, 8, 6, 4, 2>(PI, RPW, pool);
         default: return nullptr;
@@ -767,14 +853,16 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, in
     double best_time = -1.0;
     auto consider = [&](int PI, int IPW, int RPW) {
         if (!pick_s1(PI, IPW, RPW, pool)) return;
-        const int cap = kWave * PI;  // virtual pixels per image tile
+        // Virtual pixels per image tile. The last one (64*PI - 1) has no odd-tap
+        // partner, so a tile holds at most cap - 1 pixels.
+        const int cap = kWave * PI;
         int TH, nt;
-        if (img_pix <= cap) {
+        if (img_pix <= cap - 1) {
             TH = Ho;
             nt = 1;
         } else {
             if (IPW != 1) return;
-            int th_max = cap / Wp;
+            int th_max = (cap - 1) / Wp;
             if (pool) th_max &= ~1;
             if (th_max < 1) return;
             nt = ceil_div(Ho, th_max);

@@ -270,6 +270,8 @@ VARIANTS = [
     ("ipw2_rpw1_chunks", 32, 200, 520, 2, False, False, (2, 2, 1)),
     ("ipw1_rpw4_chunks_overflow", 16, 100, 520, 12, False, True, (4, 1, 4)),
     ("ipw1_rpw2_pool_chunks_overflow", 8, 100, 520, 12, True, True, (4, 1, 2)),
+    ("ipw4_rpw1_pool", 16, 3, 520, 2, True, False, (2, 4, 1)),
+    ("ipw4_rpw2_pool", 32, 3, 520, 2, True, False, (2, 4, 2)),
 ]
 
 
