@@ -10,18 +10,20 @@
 // stored), so one nonzero shifts a whole contiguous pixel range by one offset.
 //
 // Stride-1 kernel (the hot path), mapped to CDNA4:
-//  * a workgroup (4 wave64s) owns (group of IPW images, spatial tile of TH
-//    output rows at full width, tile of 4*RPW output channels); each wave owns
-//    RPW of those channels and every pixel of the tile;
+//  * a workgroup (16 wave64s, one per CU) owns (group of IPW images, spatial
+//    tile of TH output rows at full padded width, tile of 16*RPW output
+//    channels); each wave owns RPW of those channels and every pixel of the
+//    tile;
 //  * the padded input rows of the tile are copied to LDS one channel chunk at
 //    a time with asynchronous global->LDS loads into two buffers, so the copy of
 //    chunk c+1 overlaps the arithmetic on chunk c;
-//  * each wave walks its CSR rows in order; the (offset, coeff) stream arrives
-//    through scalar loads, so all lanes see the same nonzero; the tap's LDS
-//    address is decoded from the offset on the scalar unit;
-//  * lane l owns pixels l + 64*j (j < PI) of each image, so each LDS read of a
-//    wave covers 64 consecutive floats (no bank conflicts) and the epilogue's
-//    global stores are coalesced;
+//  * each wave walks its CSR rows in order: a window of entries is loaded one
+//    per lane, its offsets are decoded to LDS indices, and each entry's (index,
+//    weight) is broadcast to all lanes;
+//  * lane l owns the pixel pairs (2l + 128j, 2l+1 + 128j), so a tap is one
+//    aligned 8-byte LDS read per pair (the fastest LDS read form on gfx950);
+//    taps whose LDS index is odd are read as the pairs (2l-1, 2l) into a second
+//    accumulator set, merged with one cross-lane shift in the epilogue;
 //  * accumulators stay in VGPRs across the chunks; the epilogue adds the bias,
 //    applies ReLU and, for the pooled variant, reduces 2x2 windows through an
 //    LDS staging tile before the single store.
