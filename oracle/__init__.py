@@ -52,6 +52,11 @@ class Oracle:
         lib.oracle_conv.argtypes = [_f32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, _f32p, _u8p,
                                     ctypes.c_int, ctypes.c_int, ctypes.c_int, _f32p, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_int, ctypes.c_int, _i32p, ctypes.c_int, _f64p, _f64p, ctypes.c_int]
+        lib.oracle_conv_res.restype = ctypes.c_int
+        lib.oracle_conv_res.argtypes = [_f32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, _f32p, _u8p,
+                                        ctypes.c_int, ctypes.c_int, ctypes.c_int, _f32p, _f32p, ctypes.c_int,
+                                        ctypes.c_int, ctypes.c_int, ctypes.c_int, _i32p, ctypes.c_int, _f64p, _f64p,
+                                        ctypes.c_int]
         lib.oracle_max_threads.restype = ctypes.c_int
         lib.oracle_max_threads.argtypes = []
         self._lib = lib
@@ -81,9 +86,11 @@ class Oracle:
 
     def conv(self, x: np.ndarray, w: np.ndarray, mask: np.ndarray | None = None, bias: np.ndarray | None = None,
              stride: int = 1, pad: int = 0, relu: bool = False, pool: bool = False, pairs=None,
-             nthreads: int = 0):
-        """Fused conv -> (bias) -> ReLU -> 2x2 max-pool, in double precision.
+             nthreads: int = 0, residual: np.ndarray | None = None):
+        """Fused conv -> (bias) -> (+ residual) -> ReLU -> 2x2 max-pool, in double precision.
 
+        ``residual`` (N, K, Ho, Wo), if given, is added to the pre-activation on
+        the convolution's own grid (the shortcut of a ResNet basic block).
         Returns ``(out, absacc)``: float64 arrays of shape (N, K, Ho', Wo') or, when
         ``pairs`` (a sequence of (n, k)) is given, (len(pairs), Ho', Wo').
         """
@@ -112,9 +119,18 @@ class Oracle:
             shape = (npairs, Hq, Wq)
         out = np.zeros(shape, np.float64)
         ab = np.zeros(shape, np.float64)
-        rc = self._lib.oracle_conv(_ptr(x, _f32p), N, C, H, W, _ptr(w, _f32p), _ptr(m, _u8p), K, R, S,
-                                   _ptr(b, _f32p), stride, pad, int(bool(relu)), int(bool(pool)), _ptr(pr, _i32p),
-                                   npairs, _ptr(out, _f64p), _ptr(ab, _f64p), int(nthreads))
+        if residual is None:
+            rc = self._lib.oracle_conv(_ptr(x, _f32p), N, C, H, W, _ptr(w, _f32p), _ptr(m, _u8p), K, R, S,
+                                       _ptr(b, _f32p), stride, pad, int(bool(relu)), int(bool(pool)),
+                                       _ptr(pr, _i32p), npairs, _ptr(out, _f64p), _ptr(ab, _f64p), int(nthreads))
+        else:
+            res = np.ascontiguousarray(residual, dtype=np.float32)
+            if res.shape != (N, K, Ho, Wo):
+                raise ValueError(f"residual must have shape {(N, K, Ho, Wo)}")
+            rc = self._lib.oracle_conv_res(_ptr(x, _f32p), N, C, H, W, _ptr(w, _f32p), _ptr(m, _u8p), K, R, S,
+                                           _ptr(b, _f32p), _ptr(res, _f32p), stride, pad, int(bool(relu)),
+                                           int(bool(pool)), _ptr(pr, _i32p), npairs, _ptr(out, _f64p),
+                                           _ptr(ab, _f64p), int(nthreads))
         if rc != 0:
             raise ValueError("oracle_conv rejected the shapes")
         return out, ab

@@ -12,6 +12,7 @@
  *
  *   pre[n,k,y,x] = b[k] + sum over nonzero taps (c,r,s) of row k of
  *                  W[k,c,r,s] * Xpad[n, c, y*stride + r, x*stride + s]
+ *                  (+ res[n,k,y,x] when a residual is given)
  *   o            = relu ? max(pre, 0) : pre
  *   out          = pool ? max over a,b in {0,1} of o[n,k,2i+a,2j+b] : o
  *
@@ -22,6 +23,11 @@
  * The oracle also returns, per output, the sum of |w * x| over the same terms
  * (the max of it over the pooling window when pooling), which bounds the
  * rounding error of any fp32 evaluation order.
+ *
+ * The residual is the shortcut of a ResNet basic block (the paper's ResNet
+ * benchmark, "Evaluation"): the block input added to the second convolution's
+ * pre-activation, before its ReLU. Its magnitude is added to the sum of
+ * |w * x| of that output, since an fp32 evaluation rounds it too.
  */
 #include <math.h>
 #include <stdint.h>
@@ -78,8 +84,8 @@ static int oracle_out_extent(int in, int f, int stride, int pad) {
 
 /* One output plane (n, k): sums, activation and pooling as described above. */
 static void oracle_plane(const float *x, int C, int H, int W, const float *w, const uint8_t *mask, int R, int S,
-                         const float *bias, int stride, int pad, int relu, int pool, int n, int k,
-                         double *acc, double *ab, double *out, double *absout) {
+                         const float *bias, const float *res, int K, int stride, int pad, int relu, int pool, int n,
+                         int k, double *acc, double *ab, double *out, double *absout) {
     const int Ho = oracle_out_extent(H, R, stride, pad);
     const int Wo = oracle_out_extent(W, S, stride, pad);
     const double b = bias ? (double)bias[k] : 0.0;
@@ -106,6 +112,13 @@ static void oracle_plane(const float *x, int C, int H, int W, const float *w, co
                     }
                 }
             }
+    if (res) {
+        const float *rp = res + ((size_t)n * K + k) * Ho * Wo;
+        for (int i = 0; i < Ho * Wo; ++i) {
+            acc[i] += (double)rp[i];
+            ab[i] += fabs((double)rp[i]);
+        }
+    }
     if (relu)
         for (int i = 0; i < Ho * Wo; ++i) acc[i] = acc[i] > 0.0 ? acc[i] : 0.0;
     if (!pool) {
@@ -135,15 +148,17 @@ static void oracle_plane(const float *x, int C, int H, int W, const float *w, co
  *   x      [N][C][H][W] fp32 (unpadded)
  *   w      [K][C][R][S] fp32, mask same shape (nullable, see oracle_is_entry)
  *   bias   [K] (nullable = zero bias)
+ *   res    [N][K][Ho][Wo] (nullable = no residual), on the convolution's own
+ *          output grid (before pooling)
  *   pairs  nullable; if given, npairs (n, k) pairs, and out/absout hold one
  *          plane per pair in that order; otherwise all N*K planes, n-major.
  *   out, absout: double, plane size Ho*Wo, or (Ho/2)*(Wo/2) when pooling.
  *   nthreads: OpenMP threads (<= 0: the runtime default).
  * Returns 0, or -1 when the shapes give an empty output.
  */
-int oracle_conv(const float *x, int N, int C, int H, int W, const float *w, const uint8_t *mask, int K, int R,
-                int S, const float *bias, int stride, int pad, int relu, int pool, const int32_t *pairs,
-                int npairs, double *out, double *absout, int nthreads) {
+int oracle_conv_res(const float *x, int N, int C, int H, int W, const float *w, const uint8_t *mask, int K, int R,
+                    int S, const float *bias, const float *res, int stride, int pad, int relu, int pool,
+                    const int32_t *pairs, int npairs, double *out, double *absout, int nthreads) {
     const int Ho = oracle_out_extent(H, R, stride, pad);
     const int Wo = oracle_out_extent(W, S, stride, pad);
     if (Ho < 1 || Wo < 1) return -1;
@@ -163,13 +178,21 @@ int oracle_conv(const float *x, int N, int C, int H, int W, const float *w, cons
         for (long long p = 0; p < nplanes; ++p) {
             const int n = pairs ? pairs[2 * p] : (int)(p / K);
             const int k = pairs ? pairs[2 * p + 1] : (int)(p % K);
-            oracle_plane(x, C, H, W, w, mask, R, S, bias, stride, pad, relu, pool, n, k, acc, ab,
+            oracle_plane(x, C, H, W, w, mask, R, S, bias, res, K, stride, pad, relu, pool, n, k, acc, ab,
                          out + p * plane_out, absout + p * plane_out);
         }
         free(acc);
         free(ab);
     }
     return 0;
+}
+
+/* oracle_conv_res without a residual. */
+int oracle_conv(const float *x, int N, int C, int H, int W, const float *w, const uint8_t *mask, int K, int R,
+                int S, const float *bias, int stride, int pad, int relu, int pool, const int32_t *pairs,
+                int npairs, double *out, double *absout, int nthreads) {
+    return oracle_conv_res(x, N, C, H, W, w, mask, K, R, S, bias, NULL, stride, pad, relu, pool, pairs, npairs, out,
+                           absout, nthreads);
 }
 
 /* Number of threads the OpenMP runtime would use by default. */

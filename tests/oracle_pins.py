@@ -289,6 +289,58 @@ def pin_csr_golden(orc):
     assert vals.tolist() == g["vals"]
 
 
+def pin_library_residual(orc):
+    """With a residual (the shortcut of a ResNet basic block): oracle ==
+    float64 conv2d + bias + residual -> ReLU -> max_pool2d, the residual on the
+    convolution's own grid, added before the activation and the pool; and its
+    sum of |w*x| grows by |residual| exactly."""
+    rng = _rng(31)
+    for _ in range(25):
+        x, w, mask, bias, stride, pad = _random_case(rng)
+        w_eff = w * mask
+        N, K = x.shape[0], w.shape[0]
+        Ho = (x.shape[2] + 2 * pad - w.shape[2]) // stride + 1
+        Wo = (x.shape[3] + 2 * pad - w.shape[3]) // stride + 1
+        res = rng.uniform(-2, 2, (N, K, Ho, Wo)).astype(np.float32)
+        for relu, pool in ((False, False), (True, False), (True, True)):
+            if pool and (Ho < 2 or Wo < 2):
+                continue
+            got, ab = orc.conv(x, w, mask, bias, stride, pad, relu, pool, residual=res)
+            y = _torch_block(x, w_eff, bias, stride, pad, False, False) + res.astype(np.float64)
+            if relu:
+                y = np.maximum(y, 0.0)
+            if pool:
+                y = F.max_pool2d(torch.from_numpy(y), kernel_size=2, stride=2).numpy()
+            assert got.shape == y.shape, (got.shape, y.shape)
+            assert np.allclose(got, y, rtol=1e-12, atol=1e-12), float(np.abs(got - y).max())
+        _, ab0 = orc.conv(x, w, mask, bias, stride, pad, False, False)
+        _, ab1 = orc.conv(x, w, mask, bias, stride, pad, False, False, residual=res)
+        assert np.allclose(ab1 - ab0, np.abs(res.astype(np.float64)), rtol=0, atol=1e-12)
+
+
+def pin_residual_closed_forms(orc):
+    """Zero filter: out = relu(b + res) exactly. Identity filter (one 1.0 at
+    (c = k, centre tap), pad 1): out = relu(x + res), and pooled its 2x2 max."""
+    rng = _rng(32)
+    N, C, H, W = 2, 3, 6, 8
+    x = rng.uniform(-1, 1, (N, C, H, W)).astype(np.float32)
+    res = rng.uniform(-1, 1, (N, C, H, W)).astype(np.float32)
+    b = rng.uniform(-0.5, 0.5, C).astype(np.float32)
+    w0 = np.zeros((C, C, 3, 3), np.float32)
+    got, _ = orc.conv(x, w0, None, b, 1, 1, True, False, residual=res)
+    want = np.maximum(b[None, :, None, None].astype(np.float64) + res, 0.0)
+    assert np.array_equal(got, want)
+    wi = np.zeros((C, C, 3, 3), np.float32)
+    for k in range(C):
+        wi[k, k, 1, 1] = 1.0
+    got, _ = orc.conv(x, wi, None, None, 1, 1, True, False, residual=res)
+    want = np.maximum(x.astype(np.float64) + res.astype(np.float64), 0.0)
+    assert np.array_equal(got, want)
+    gp, _ = orc.conv(x, wi, None, None, 1, 1, True, True, residual=res)
+    wp = want.reshape(N, C, H // 2, 2, W // 2, 2).max(axis=(3, 5))
+    assert np.array_equal(gp, wp)
+
+
 ALL_PINS = [
     pin_library_conv,
     pin_library_absacc,
@@ -302,4 +354,6 @@ ALL_PINS = [
     pin_csr_library,
     pin_csr_offsets,
     pin_csr_golden,
+    pin_library_residual,
+    pin_residual_closed_forms,
 ]

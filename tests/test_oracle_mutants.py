@@ -33,6 +33,10 @@ MUTANTS = {
                            "offset[nnz] = (int32_t)(c * Wp * Wp + r * Wp + s);"),
     "colidx_transposed": ("colidx[nnz] = (int32_t)((c * R + r) * S + s);",
                           "colidx[nnz] = (int32_t)((c * S + s) * R + r);"),
+    "residual_dropped": ("acc[i] += (double)rp[i];", "(void)rp[i];"),
+    "residual_after_relu": ("    if (res) {\n        const float *rp", "    if (relu)\n        for (int i = 0; i < Ho * Wo; ++i) acc[i] = acc[i] > 0.0 ? acc[i] : 0.0;\n    if (res) {\n        const float *rp"),
+    "residual_batch_ignored": ("const float *rp = res + ((size_t)n * K + k) * Ho * Wo;", "const float *rp = res + ((size_t)k) * Ho * Wo;"),
+    "residual_sign": ("acc[i] += (double)rp[i];", "acc[i] -= (double)rp[i];"),
     "pack_last_row_dropped": ("for (int k = 0; k < K; ++k) {\n        for (int c = 0; c < C; ++c)\n            for (int r = 0; r < R; ++r)\n                for (int s = 0; s < S; ++s) {\n                    size_t i",
                               "for (int k = 0; k < K - 1; ++k) {\n        for (int c = 0; c < C; ++c)\n            for (int r = 0; r < R; ++r)\n                for (int s = 0; s < S; ++s) {\n                    size_t i"),
 }
