@@ -133,6 +133,53 @@ int spconv_pad_input(const float *in, int N, int C, int H, int W, int pad, float
 int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S,
                    int stride, int pad, const float *bias, uint32_t flags, float *out, hipStream_t stream);
 
+/*
+ * Epilogue options of spconv_forward_ex: where the fused output goes and what is
+ * added before the activation. A zero-initialised struct gives spconv_forward's
+ * behaviour.
+ *
+ * out_pad   >= 0. The stored output planes carry a border of out_pad zeros:
+ *           out is [N][K][Hs+2*out_pad][Ws+2*out_pad] (Hs x Ws the stored plane:
+ *           Ho x Wo, or Ho/2 x Wo/2 pooled), the value of (n,k,i,j) at row
+ *           i+out_pad, column j+out_pad, and every border element is written
+ *           with +0.0 by the same launch. With out_pad equal to the next
+ *           layer's pad, out is that layer's in_padded: the zero-padding pass
+ *           between chained layers disappears (the paper fuses consecutive
+ *           operators, "Evaluation").
+ * residual  nullable, device. A tensor on the convolution's own output grid,
+ *           added to the pre-activation before ReLU and pooling:
+ *             pre[n,k,y,x] += residual[n][k][y+residual_pad][x+residual_pad]
+ *           over planes of (Ho+2*residual_pad) x (Wo+2*residual_pad). This is
+ *           the shortcut of a ResNet basic block (the paper's ResNet benchmark,
+ *           "Evaluation"), read straight from a padded block input when
+ *           residual_pad equals that input's pad. Must not overlap out.
+ * residual_pad >= 0, ignored without a residual.
+ * Both borders are limited so that one padded plane has fewer than 2^31
+ * elements.
+ */
+typedef struct spconv_epilogue {
+    int32_t out_pad;
+    int32_t residual_pad;
+    const float *residual;
+} spconv_epilogue;
+
+/*
+ * spconv_forward_ex - spconv_forward with epilogue options (device, asynchronous,
+ * one kernel, one store per output element including the border).
+ *
+ *   pre = bias[k] + sum_j vals[j] * in_padded[...]      (as spconv_forward)
+ *         + residual[n,k,y,x]                           (epi->residual != NULL)
+ *   o   = RELU ? max(pre, 0) : pre;   q = MAXPOOL2X2 ? 2x2 max of o : o
+ *   out[n][k][i+out_pad][j+out_pad] = q[n,k,i,j];  border of out = +0.0
+ *
+ * epi: host struct, nullable (= all zero). Other arguments, layouts and errors
+ * as spconv_forward; additionally SPCONV_EINVAL for a negative out_pad or
+ * residual_pad, or a padded output or residual plane of 2^31 elements or more.
+ */
+int spconv_forward_ex(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S,
+                      int stride, int pad, const float *bias, uint32_t flags, const spconv_epilogue *epi, float *out,
+                      hipStream_t stream);
+
 /* Kernel families reported by spconv_plan. */
 #define SPCONV_KERNEL_STRIDE1 1 /* stride 1: channel-chunked LDS staging, lanes own padded-width pixels */
 #define SPCONV_KERNEL_GENERIC 2 /* any stride */

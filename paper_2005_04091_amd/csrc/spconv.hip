@@ -159,7 +159,38 @@ struct FwdArgs {
     uint32_t magic;    // c = offset / (Hp*Wp) == (offset * magic) >> shift
     int shift;
     int plane_delta;   // Hp*Wp - PL
+    // epilogue: stored planes carry a zero border of out_pad (pitch opitch,
+    // oplane elements each); the residual planes a border of res_pad (pitch
+    // rpitch, rplane elements each)
+    int out_pad, opitch;
+    size_t oplane;
+    int res_pad, rpitch;
+    size_t rplane;
 };
+
+// Zero the border of one stored output plane (Hs x Ws inside a border of pd,
+// row pitch `pitch`) for a tile of stored rows [r0, r1): the left and right
+// border columns of those rows, and the top border rows when the tile is the
+// first of the plane, the bottom ones when it is the last. The tiles of a
+// plane partition its rows, so every border element is written exactly once.
+__device__ __forceinline__ void zero_border(float *plane, int r0, int r1, int Hs, int Ws, int pd, int pitch,
+                                            bool first, bool last, int lane, int nlanes) {
+    const int side = (r1 - r0) * 2 * pd;
+    const int top = first ? pd * pitch : 0;
+    const int bottom = last ? pd * pitch : 0;
+    for (int t = lane; t < side + top + bottom; t += nlanes) {
+        int idx;
+        if (t < side) {
+            const int rr = t / (2 * pd), c = t - rr * 2 * pd;
+            idx = (r0 + rr + pd) * pitch + (c < pd ? c : Ws + c);
+        } else if (t < side + top) {
+            idx = t - side;
+        } else {
+            idx = (pd + Hs) * pitch + (t - side - top);
+        }
+        plane[idx] = 0.0f;
+    }
+}
 
 // Workgroup id -> linear work index such that consecutive work items (the
 // channel tiles of one image tile, which read the same input rows) land on the
@@ -406,7 +437,8 @@ __device__ __forceinline__ void merge_pairs(const float2 (&e)[PJ], const float2 
 template <int PI, int IPW, int RPW, bool POOL>
 __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4))) void spconv_s1_kernel(
     FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ offset,
-    const float *__restrict__ vals, const float *__restrict__ bias, float *__restrict__ out) {
+    const float *__restrict__ vals, const float *__restrict__ bias, const float *__restrict__ res,
+    float *__restrict__ out) {
     extern __shared__ float lds[];
     constexpr int KT = RPW * kS1Waves;  // output channels per workgroup
     constexpr int PJ = PI / 2;          // pixel pairs per lane per image
@@ -527,16 +559,19 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 
     const int tile_px = a.TH * a.Wp;
     if constexpr (!POOL) {
-        int pix[PJ][2];  // in-plane output index of each of this lane's pixels, or -1
+        // Tile row of each of this lane's pixels, or -1 when the pixel is not
+        // stored. Pixel qq = yl*Wp + x of the tile lands at qq + yl*(pitch - Wp)
+        // past the tile's first element, in the output and the residual alike.
+        int ylo[PJ][2];
 #pragma unroll
         for (int p = 0; p < PJ; ++p)
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int qq = q + 2 * kWave * p + h;
                 const int yl = qq / a.Wp, x = qq - yl * a.Wp;
-                const int y = y0 + yl;
-                pix[p][h] = (qq < tile_px && x < a.Wo && y < a.Ho) ? y * a.Wo + x : -1;
+                ylo[p][h] = (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) ? yl : -1;
             }
+        const int odelta = a.opitch - a.Wp, rdelta = a.rpitch - a.Wp;
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             const int k = krow[i];
@@ -546,19 +581,28 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
             for (int im = 0; im < IPW; ++im) {
                 const int n = ig * IPW + im;
                 if (n >= a.N) break;
-                float *op = out + ((size_t)n * a.K + k) * (size_t)a.Ho * a.Wo;
+                float *plane = out + ((size_t)n * a.K + k) * a.oplane;
+                float *op = plane + (size_t)(y0 + a.out_pad) * a.opitch + a.out_pad;
+                const float *rp =
+                    res ? res + ((size_t)n * a.K + k) * a.rplane + (size_t)(y0 + a.res_pad) * a.rpitch + a.res_pad
+                        : nullptr;
                 float2 sum[PJ];
                 merge_pairs(accE[i][im], accO[i][im], sum, lane);
 #pragma unroll
-                for (int p = 0; p < PJ; ++p) {
-                    float v0 = sum[p].x + bk, v1 = sum[p].y + bk;
-                    if (a.relu) {
-                        v0 = v0 > 0.0f ? v0 : 0.0f;
-                        v1 = v1 > 0.0f ? v1 : 0.0f;
+                for (int p = 0; p < PJ; ++p)
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int yl = ylo[p][h];
+                        if (yl < 0) continue;
+                        const int qq = q + 2 * kWave * p + h;
+                        float v = (h ? sum[p].y : sum[p].x) + bk;
+                        if (rp) v += rp[qq + yl * rdelta];
+                        if (a.relu) v = v > 0.0f ? v : 0.0f;
+                        op[qq + yl * odelta] = v;
                     }
-                    if (pix[p][0] >= 0) op[pix[p][0]] = v0;
-                    if (pix[p][1] >= 0) op[pix[p][1]] = v1;
-                }
+                if (a.out_pad)
+                    zero_border(plane, y0, min(y0 + a.TH, a.Ho), a.Ho, a.Wo, a.out_pad, a.opitch, ty == 0,
+                                ty == a.ntiles_y - 1, lane, kWave);
             }
         }
     } else {
@@ -580,14 +624,29 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
             for (int im = 0; im < IPW; ++im) {
                 float2 sum[PJ];
                 merge_pairs(accE[i][im], accO[i][im], sum, lane);
+                const int n = ig * IPW + im;
+                // The residual is added on the convolution's grid, before the
+                // activation and the pool; pixels outside the plane get none.
+                const float *rp = (res && k < a.K && n < a.N)
+                                      ? res + ((size_t)n * a.K + k) * a.rplane +
+                                            (size_t)(y0 + a.res_pad) * a.rpitch + a.res_pad
+                                      : nullptr;
 #pragma unroll
                 for (int p = 0; p < PJ; ++p) {
-                    float v0 = sum[p].x + bk, v1 = sum[p].y + bk;
-                    if (a.relu) {
-                        v0 = v0 > 0.0f ? v0 : 0.0f;
-                        v1 = v1 > 0.0f ? v1 : 0.0f;
+                    float v[2] = {sum[p].x + bk, sum[p].y + bk};
+                    if (rp) {
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            const int qq = q + 2 * kWave * p + h;
+                            const int yl = qq / a.Wp, x = qq - yl * a.Wp;
+                            if (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) v[h] += rp[qq + yl * (a.rpitch - a.Wp)];
+                        }
                     }
-                    *reinterpret_cast<float2 *>(st + im * kImgPx + q + 2 * kWave * p) = make_float2(v0, v1);
+                    if (a.relu) {
+                        v[0] = v[0] > 0.0f ? v[0] : 0.0f;
+                        v[1] = v[1] > 0.0f ? v[1] : 0.0f;
+                    }
+                    *reinterpret_cast<float2 *>(st + im * kImgPx + q + 2 * kWave * p) = make_float2(v[0], v[1]);
                 }
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the whole tile is staged
@@ -602,9 +661,17 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
                     if (n < a.N && pr < a.Hq) {
                         const float *s0 = st + im * kImgPx + (2 * r) * a.Wp + 2 * jq;
                         const float m = fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[a.Wp], s0[a.Wp + 1]));
-                        out[((size_t)n * a.K + k) * (size_t)a.Hq * a.Wq + (size_t)pr * a.Wq + jq] = m;
+                        out[((size_t)n * a.K + k) * a.oplane + (size_t)(pr + a.out_pad) * a.opitch + jq + a.out_pad] =
+                            m;
                     }
                 }
+                if (a.out_pad)
+                    for (int im = 0; im < IPW; ++im) {
+                        const int n = ig * IPW + im;
+                        if (n >= a.N) break;
+                        zero_border(out + ((size_t)n * a.K + k) * a.oplane, prow0, min(prow0 + prows, a.Hq), a.Hq,
+                                    a.Wq, a.out_pad, a.opitch, ty == 0, ty == a.ntiles_y - 1, lane, kWave);
+                    }
             }
         }
     }
@@ -615,9 +682,13 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 // x*stride), so a nonzero costs one address add per pixel. Correct for any
 // stride; the stride-1 kernel above is the fast path.
 template <int P, int KT, bool POOL>
-__global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr,
-                                                         const int32_t *__restrict__ offset, const float *__restrict__ vals,
-                                                         const float *__restrict__ bias, float *__restrict__ out) {
+__global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, const float *__restrict__ xp,
+                                                                  const int32_t *__restrict__ rowptr,
+                                                                  const int32_t *__restrict__ offset,
+                                                                  const float *__restrict__ vals,
+                                                                  const float *__restrict__ bias,
+                                                                  const float *__restrict__ res,
+                                                                  float *__restrict__ out) {
     extern __shared__ float lds[];
 
     const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
@@ -692,28 +763,42 @@ __global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, con
         }
     }
 
+    // Tile row of each of this lane's pixels, or -1 when the pixel is not
+    // stored; pixel q = yl*wv + x of the tile lands at q + yl*(pitch - wv) past
+    // the tile's first element, in the output and the residual alike.
+    int ylo[P];
+#pragma unroll
+    for (int j = 0; j < P; ++j) {
+        const int q = qw + kWave * j;
+        const int yl = q / a.wv, x = q - yl * a.wv;
+        ylo[j] = (q < tile_px && x < a.Wo && y0 + yl < a.Ho) ? yl : -1;
+    }
+    const int rdelta = a.rpitch - a.wv;
     if constexpr (!POOL) {
         if (!active) return;
-        int pix[P];
-#pragma unroll
-        for (int j = 0; j < P; ++j) {
-            const int q = qw + kWave * j;
-            const int yl = q / a.wv, x = q - yl * a.wv;
-            const int y = y0 + yl;
-            pix[j] = (q < tile_px && x < a.Wo && y < a.Ho) ? y * a.Wo + x : -1;
-        }
+        const int odelta = a.opitch - a.wv;
 #pragma unroll
         for (int kk = 0; kk < KT; ++kk) {
             const int k = k0 + kk;
             if (k >= a.K) break;
             const float bk = bias ? bias[k] : 0.0f;
-            float *op = out + ((size_t)n * a.K + k) * (size_t)a.Ho * a.Wo;
+            float *plane = out + ((size_t)n * a.K + k) * a.oplane;
+            float *op = plane + (size_t)(y0 + a.out_pad) * a.opitch + a.out_pad;
+            const float *rp =
+                res ? res + ((size_t)n * a.K + k) * a.rplane + (size_t)(y0 + a.res_pad) * a.rpitch + a.res_pad
+                    : nullptr;
 #pragma unroll
             for (int j = 0; j < P; ++j) {
+                if (ylo[j] < 0) continue;
+                const int q = qw + kWave * j;
                 float v = acc[kk][j] + bk;
+                if (rp) v += rp[q + ylo[j] * rdelta];
                 if (a.relu) v = v > 0.0f ? v : 0.0f;
-                if (pix[j] >= 0) op[pix[j]] = v;
+                op[q + ylo[j] * odelta] = v;
             }
+            if (a.out_pad && wseg == 0)
+                zero_border(plane, y0, min(y0 + a.TH, a.Ho), a.Ho, a.Wo, a.out_pad, a.opitch, ty == 0,
+                            ty == a.ntiles_y - 1, lane, kWave);
         }
     } else {
         const int img_px = a.wpi * kWave * P;
@@ -727,9 +812,15 @@ __global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, con
             if (k >= a.K) break;
             const float bk = bias ? bias[k] : 0.0f;
             __syncthreads();  // previous readers of the staging area are done
+            // The residual is added on the convolution's grid, before the
+            // activation and the pool.
+            const float *rp = (res && active) ? res + ((size_t)n * a.K + k) * a.rplane +
+                                                    (size_t)(y0 + a.res_pad) * a.rpitch + a.res_pad
+                                              : nullptr;
 #pragma unroll
             for (int j = 0; j < P; ++j) {
                 float v = acc[kk][j] + bk;
+                if (rp && ylo[j] >= 0) v += rp[qw + kWave * j + ylo[j] * rdelta];
                 if (a.relu) v = v > 0.0f ? v : 0.0f;
                 lds[img * img_px + qw + kWave * j] = v;
             }
@@ -744,9 +835,16 @@ __global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, con
                 if (nn < a.N && pi < a.Hq) {
                     const float *s0 = lds + im * img_px + (2 * i) * a.wv + 2 * jq;
                     const float m = fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[a.wv], s0[a.wv + 1]));
-                    out[((size_t)nn * a.K + k) * (size_t)a.Hq * a.Wq + (size_t)pi * a.Wq + jq] = m;
+                    out[((size_t)nn * a.K + k) * a.oplane + (size_t)(pi + a.out_pad) * a.opitch + jq + a.out_pad] = m;
                 }
             }
+            if (a.out_pad)
+                for (int im = 0; im < a.ipw; ++im) {
+                    const int nn = ig * a.ipw + im;
+                    if (nn >= a.N) break;
+                    zero_border(out + ((size_t)nn * a.K + k) * a.oplane, prow0, min(prow0 + prows, a.Hq), a.Hq, a.Wq,
+                                a.out_pad, a.opitch, ty == 0, ty == a.ntiles_y - 1, (int)threadIdx.x, kThreads);
+                }
         }
     }
 }
@@ -789,7 +887,7 @@ struct Plan {
 };
 
 using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_t *, const float *, const float *,
-                          float *);
+                          const float *, float *);
 
 template <int PI, int IPW>
 FwdKernel pick_s1_rpw(int RPW, bool pool) {
@@ -1120,21 +1218,48 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     // Both kernels address a staged channel at its LDS pitch: PLp (stride 1) or PL.
     a.plane_delta = (int)(Hp * Wp) - (pl.kind == Kind::kStride1 ? pl.PLp : pl.PL);
     if (!pick_kernel(pl, pool)) return SPCONV_EINVAL;
+    // Epilogue defaults: dense output planes, no residual.
+    a.out_pad = 0;
+    a.opitch = a.Wq;
+    a.oplane = (size_t)a.Hq * a.Wq;
+    a.res_pad = 0;
+    a.rpitch = a.Wo;
+    a.rplane = (size_t)a.Ho * a.Wo;
     *plp = pl;
     *ap = a;
     return SPCONV_OK;
 }
 
+// Epilogue options of spconv_forward_ex, checked and folded into the args.
+int apply_epilogue(const spconv_epilogue *epi, FwdArgs *a) {
+    if (!epi) return SPCONV_OK;
+    if (epi->out_pad < 0 || (epi->residual && epi->residual_pad < 0)) return SPCONV_EINVAL;
+    const long long op = epi->out_pad, rp = epi->residual ? epi->residual_pad : 0;
+    const long long oh = a->Hq + 2 * op, ow = a->Wq + 2 * op;
+    const long long rh = a->Ho + 2 * rp, rw = a->Wo + 2 * rp;
+    if (oh * ow >= (1LL << 31) || rh * rw >= (1LL << 31)) return SPCONV_EINVAL;
+    a->out_pad = (int)op;
+    a->opitch = (int)ow;
+    a->oplane = (size_t)(oh * ow);
+    a->res_pad = (int)rp;
+    a->rpitch = (int)rw;
+    a->rplane = (size_t)(rh * rw);
+    return SPCONV_OK;
+}
+
 }  // namespace
 
-extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R,
-                              int S, int stride, int pad, const float *bias, uint32_t flags, float *out,
-                              hipStream_t stream) {
+extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K,
+                                 int R, int S, int stride, int pad, const float *bias, uint32_t flags,
+                                 const spconv_epilogue *epi, float *out, hipStream_t stream) {
     if (!in_padded || !out) return SPCONV_EINVAL;
     Plan pl;
     FwdArgs a;
-    const int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, &pl, &a);
+    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, &pl, &a);
     if (rc != SPCONV_OK) return rc;
+    rc = apply_epilogue(epi, &a);
+    if (rc != SPCONV_OK) return rc;
+    const float *residual = epi ? epi->residual : nullptr;
     FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0);
     const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
     if (pl.lds_bytes > 65536 &&
@@ -1142,8 +1267,14 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
             hipSuccess)
         return SPCONV_EHIP;
     hipLaunchKernelGGL(kern, dim3((unsigned)pl.total_wgs), dim3(threads), pl.lds_bytes, stream, a, in_padded,
-                       csr->rowptr, csr->offset, csr->vals, bias, out);
+                       csr->rowptr, csr->offset, csr->vals, bias, residual, out);
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
+extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R,
+                              int S, int stride, int pad, const float *bias, uint32_t flags, float *out,
+                              hipStream_t stream) {
+    return spconv_forward_ex(in_padded, N, C, H, W, csr, K, R, S, stride, pad, bias, flags, nullptr, out, stream);
 }
 
 extern "C" int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride,

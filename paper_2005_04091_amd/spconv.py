@@ -24,8 +24,8 @@ SPCONV_EHIP = -3
 SPCONV_RELU = 1
 SPCONV_MAXPOOL2X2 = 2
 
-EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_plan", "spconv_output_shape",
-            "spconv_strerror")
+EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
+            "spconv_output_shape", "spconv_strerror")
 SPCONV_KERNEL_STRIDE1 = 1
 SPCONV_KERNEL_GENERIC = 2
 
@@ -36,6 +36,11 @@ class spconv_csr(ctypes.Structure):
                 ("Hp", ctypes.c_int32), ("Wp", ctypes.c_int32), ("nnz", ctypes.c_int64),
                 ("rowptr", ctypes.c_void_p), ("colidx", ctypes.c_void_p), ("offset", ctypes.c_void_p),
                 ("vals", ctypes.c_void_p), ("max_row_nnz", ctypes.c_int64)]
+
+
+class spconv_epilogue(ctypes.Structure):
+    """Mirror of ``struct spconv_epilogue``."""
+    _fields_ = [("out_pad", ctypes.c_int32), ("residual_pad", ctypes.c_int32), ("residual", ctypes.c_void_p)]
 
 
 class spconv_plan_info(ctypes.Structure):
@@ -61,6 +66,10 @@ def _bind(lib):
     lib.spconv_forward.restype = _c_int
     lib.spconv_forward.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int,
                                    _c_int, _c_int, _c_int, _vp, ctypes.c_uint32, _vp, _vp]
+    lib.spconv_forward_ex.restype = _c_int
+    lib.spconv_forward_ex.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int,
+                                      _c_int, _c_int, _c_int, _c_int, _vp, ctypes.c_uint32,
+                                      ctypes.POINTER(spconv_epilogue), _vp, _vp]
     lib.spconv_plan.restype = _c_int
     lib.spconv_plan.argtypes = [_c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int, _c_int,
                                 _c_int, _c_int, ctypes.c_uint32, ctypes.POINTER(spconv_plan_info)]
@@ -204,6 +213,24 @@ def spconv_forward(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R
     return out
 
 
+def spconv_forward_ex(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int,
+                      pad: int, bias=None, flags: int = SPCONV_RELU, out_pad: int = 0, residual=None,
+                      residual_pad: int = 0, out=None, stream=None):
+    """``spconv_forward`` with epilogue options: the stored planes get a zero
+    border of ``out_pad`` (the next layer's padded input), and ``residual`` (on
+    the convolution's grid, with a border of ``residual_pad``) is added before
+    the activation."""
+    import torch
+    Hs, Ws = spconv_output_shape(H, W, R, S, stride, pad, flags)
+    if out is None:
+        out = torch.empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), dtype=torch.float32, device=xp.device)
+    epi = spconv_epilogue(out_pad, residual_pad, _dev_ptr(residual, "residual"))
+    _check(_lib.spconv_forward_ex(_dev_ptr(xp, "xp"), N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad,
+                                  _dev_ptr(bias, "bias"), flags, ctypes.byref(epi), _dev_ptr(out, "out"),
+                                  _stream_handle(stream, xp.device)), "spconv_forward_ex")
+    return out
+
+
 def spconv_plan(N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int, pad: int,
                 flags: int = SPCONV_RELU) -> dict:
     """The launch plan ``spconv_forward`` would use, as a dict of the
@@ -239,10 +266,18 @@ class SparseConvLayer:
     def pad_input(self, x, out=None, stream=None):
         return spconv_pad_input(x, self.pad, out=out, stream=stream)
 
-    def forward_padded(self, xp, out=None, stream=None):
+    def forward_padded(self, xp, out=None, stream=None, out_pad: int = 0, residual=None, residual_pad: int = 0):
+        """Fused forward on the padded input. With ``out_pad`` the output planes
+        carry that zero border (ready as the next layer's padded input); with
+        ``residual`` (border ``residual_pad``) the shortcut is added before the
+        activation."""
         N = int(xp.shape[0])
-        return spconv_forward(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
-                              self.pad, self.bias, self.flags, out=out, stream=stream)
+        if out_pad == 0 and residual is None:
+            return spconv_forward(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
+                                  self.pad, self.bias, self.flags, out=out, stream=stream)
+        return spconv_forward_ex(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
+                                 self.pad, self.bias, self.flags, out_pad=out_pad, residual=residual,
+                                 residual_pad=residual_pad, out=out, stream=stream)
 
     def plan(self, N: int) -> dict:
         return spconv_plan(N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride, self.pad,

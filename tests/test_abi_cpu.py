@@ -34,8 +34,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(
-        ["spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_plan", "spconv_output_shape",
-         "spconv_strerror"])
+        ["spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
+         "spconv_output_shape", "spconv_strerror"])
 
 
 def test_library_exports_every_declared_symbol(sp):
@@ -186,6 +186,21 @@ def test_forward_and_pad_validate_before_any_gpu_work(sp):
         assert fwd(csr=sp.spconv_csr(4, 3, 3, 3, 10, 12, 5, fake, fake, fake, fake, bad_hint)) == E
     tiny = sp.spconv_csr(4, 3, 3, 3, 3, 3, 5, fake, fake, fake, fake)
     assert fwd(csr=tiny, H=3, W=3, pad=0, flags=sp.SPCONV_MAXPOOL2X2) == E  # 1x1 output cannot be pooled
+    # epilogue options are checked on the host as well
+    def fwd_ex(out_pad=0, residual_pad=0, residual=None, **kw):
+        a = dict(ok)
+        a.update(kw)
+        epi = sp.spconv_epilogue(out_pad, residual_pad, residual)
+        return lib.spconv_forward_ex(a["xp"], a["N"], a["C"], a["H"], a["W"], ctypes.byref(csr), a["K"], a["R"],
+                                     a["S"], a["stride"], a["pad"], a["bias"], a["flags"], ctypes.byref(epi),
+                                     a["out"], None)
+
+    assert fwd_ex(out_pad=-1) == E
+    assert fwd_ex(residual=fake, residual_pad=-1) == E
+    assert fwd_ex(out_pad=1 << 16) == E            # padded output plane of 2^31 elements or more
+    assert fwd_ex(residual=fake, residual_pad=1 << 16) == E
+    assert fwd_ex(out=None, out_pad=1) == E
+    assert fwd_ex(N=0, out_pad=1) == E
     assert lib.spconv_pad_input(None, 1, 1, 4, 4, 1, fake, None) == E
     assert lib.spconv_pad_input(fake, 1, 1, 0, 4, 1, fake, None) == E
     assert lib.spconv_pad_input(fake, 1, 1, 4, 4, -1, fake, None) == E
