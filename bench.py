@@ -33,6 +33,13 @@ WORKLOADS = {
     "narrow_d0.2": "deep narrow: N=32, C=K=256, 14x14, 3x3, density 0.2 (Beta(2,5) row skew), bias+ReLU, fp32",
     "narrow_d0.5": "deep narrow: N=32, C=K=256, 14x14, 3x3, density 0.5 (Beta(2,5) row skew), bias+ReLU, fp32",
 }
+# Chained blocks: several layers per step, fused through zero-bordered outputs.
+BLOCKS = {
+    "vgg_block": "VGG-style block: N=32, C=3 padded to 64, 224x224, two chained 3x3 convs C=K=64, density 0.2, "
+                 "bias+ReLU, the second with 2x2 max-pool; fp32",
+    "resnet_block": "ResNet basic block: N=32, C=K=64, 56x56, relu(conv2(relu(conv1(x))) + x), 3x3 convs, "
+                    "density 0.2, bias; fp32",
+}
 
 
 def algorithmic(layer, nnz):
@@ -131,12 +138,83 @@ def cpu_baseline(layer, budget_s: float):
     return {"value": flops / dt / 1e9, "unit": "GFLOP/s", "cores": threads, "kind": "oracle", "sample": sample}
 
 
+def bench_block(args, dev):
+    """A chained block per step, with inputs resident in HBM: the input is
+    padded once, layer 1 writes layer 2's padded input directly (zero border),
+    layer 2 reads the shortcut from the padded block input (ResNet block). The
+    same block with a separate padding pass between the layers (`unfused`) is
+    timed right after, on the same buffers."""
+    import torch
+
+    from paper_2005_04091_amd import spconv, synth
+
+    x, l1, l2 = synth.make_vgg_block() if args.workload == "vgg_block" else synth.make_resnet_block()
+    resnet = args.workload == "resnet_block"
+    N, C, H, W, K, R, S = l1.shape
+    L1 = spconv.SparseConvLayer(l1.w, l1.mask, l1.bias, H, W, 1, 1, True, False, device=dev)
+    L2 = spconv.SparseConvLayer(l2.w, l2.mask, l2.bias, H, W, 1, 1, True, l2.pool, device=dev)
+    xd = torch.from_numpy(x).to(dev)
+    xp = torch.empty((N, C, H + 2, W + 2), dtype=torch.float32, device=dev)
+    y1 = torch.empty((N, K, H, W), dtype=torch.float32, device=dev)
+    y1p = torch.empty((N, K, H + 2, W + 2), dtype=torch.float32, device=dev)
+    y2 = torch.empty((N, K, L2.Ho, L2.Wo), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    res = dict(residual=xp, residual_pad=1) if resnet else {}
+
+    def fused():
+        L1.pad_input(xd, out=xp, stream=stream)
+        L1.forward_padded(xp, out=y1p, stream=stream, out_pad=1)
+        L2.forward_padded(y1p, out=y2, stream=stream, **res)
+
+    def unfused():
+        L1.pad_input(xd, out=xp, stream=stream)
+        L1.forward_padded(xp, out=y1, stream=stream)
+        L2.pad_input(y1, out=y1p, stream=stream)
+        L2.forward_padded(y1p, out=y2, stream=stream, **res)
+
+    def timed(step):
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    ms = timed(fused)
+    ms_unfused = timed(unfused)
+    nnz1, nnz2 = L1.host_csr.nnz, L2.host_csr.nnz
+    flops = 2.0 * (nnz1 + nnz2) * N * H * W
+    rec = {
+        "metric": "ms/layer + nonzero GFLOP/s + % HBM roofline, fused sparse conv, 1 MI355X",
+        "value": round(flops / (ms * 1e-3) / 1e9, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Bernoulli-masked weights U[-1,1), input U[0,1), bias U[-0.1,0.1))",
+        "config": {"workload": BLOCKS[args.workload], "N": N, "C": C, "K": K, "H": H, "W": W,
+                   "nnz": [nnz1, nnz2], "pool": bool(l2.pool), "residual": resnet},
+        "ms_per_step_unfused": round(ms_unfused, 5),
+        "fusion_saving_frac": round(1.0 - ms / ms_unfused, 4),
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="resnet", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="resnet", choices=sorted(WORKLOADS) + sorted(BLOCKS))
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -156,6 +234,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.workload in BLOCKS:
+        bench_block(args, dev)
+        return
     layer = synth.make_layer(args.workload)
     N, C, H, W, K, R, S = layer.shape
     print(f"[bench] workload {args.workload}: {WORKLOADS[args.workload]}", file=sys.stderr, flush=True)

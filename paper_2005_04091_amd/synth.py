@@ -128,6 +128,31 @@ def make_vgg_block():
     return x, l1, l2
 
 
+# A ResNet basic block at the ResNet layer's shape: relu(conv2(relu(conv1(x))) + x).
+RESNET_BLOCK = dict(N=32, C=64, H=56, W=56, density=0.2, seed=SEED_BASE + 6)
+
+
+def make_resnet_block():
+    """Input and the two layers of a ResNet basic block (the shortcut is the
+    block input, added before the second layer's ReLU). Draw order: mask 1,
+    mask 2, weights 1, weights 2, input, bias 1, bias 2. Returns ``(x, layer1,
+    layer2)``; layer 2's ``x`` is a seeded U[0, 1) tensor of its input shape."""
+    cfg = RESNET_BLOCK
+    rng = np.random.default_rng(cfg["seed"])
+    N, C, H, W, d = cfg["N"], cfg["C"], cfg["H"], cfg["W"], cfg["density"]
+    m1 = _mask(rng, C, C, 3, 3, d)
+    m2 = _mask(rng, C, C, 3, 3, d)
+    w1 = _weights(rng, m1)
+    w2 = _weights(rng, m2)
+    x = _input(rng, N, C, H, W)
+    b1 = _bias(rng, C)
+    b2 = _bias(rng, C)
+    x2 = _input(rng, N, C, H, W)
+    l1 = Layer("resnet_block_conv1", x, w1, m1, b1, stride=1, pad=1, relu=True, pool=False)
+    l2 = Layer("resnet_block_conv2", x2, w2, m2, b2, stride=1, pad=1, relu=True, pool=False)
+    return x, l1, l2
+
+
 def random_layer(seed: int, N: int, C: int, K: int, H: int, W: int, R: int = 3, S: int = 3, stride: int = 1,
                  pad: int = 1, density: float = 0.2, relu: bool = True, pool: bool = False, bias: bool = True,
                  skew: bool = False) -> Layer:
