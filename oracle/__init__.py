@@ -57,6 +57,9 @@ class Oracle:
                                         ctypes.c_int, ctypes.c_int, ctypes.c_int, _f32p, _f32p, ctypes.c_int,
                                         ctypes.c_int, ctypes.c_int, ctypes.c_int, _i32p, ctypes.c_int, _f64p, _f64p,
                                         ctypes.c_int]
+        lib.oracle_resize_bilinear.restype = None
+        lib.oracle_resize_bilinear.argtypes = [_f32p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                               ctypes.c_int, ctypes.c_int, _f64p, _f64p]
         lib.oracle_max_threads.restype = ctypes.c_int
         lib.oracle_max_threads.argtypes = []
         self._lib = lib
@@ -135,6 +138,18 @@ class Oracle:
             raise ValueError("oracle_conv rejected the shapes")
         return out, ab
 
+    def resize(self, x: np.ndarray, H: int, W: int):
+        """Bilinear resize (half-pixel centres, clamped at the borders) of NCHW
+        ``x`` to H x W, in double. Returns ``(out, absacc)``."""
+        x = np.ascontiguousarray(x, dtype=np.float32)
+        N, C, Hin, Win = x.shape
+        if min(N, C, Hin, Win, H, W) < 1:
+            raise ValueError("empty resize")
+        out = np.zeros((N, C, H, W), np.float64)
+        ab = np.zeros((N, C, H, W), np.float64)
+        self._lib.oracle_resize_bilinear(_ptr(x, _f32p), N, C, Hin, Win, H, W, _ptr(out, _f64p), _ptr(ab, _f64p))
+        return out, ab
+
     @staticmethod
     def pad(x: np.ndarray, pad: int) -> np.ndarray:
         """Zero-padded NCHW copy (the padded input the CSR offsets index)."""
@@ -170,3 +185,7 @@ def conv(*a, **k):
 
 def pad(x, p):
     return Oracle.pad(x, p)
+
+
+def resize(*a, **k):
+    return get().resize(*a, **k)

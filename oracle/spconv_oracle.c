@@ -187,6 +187,46 @@ int oracle_conv_res(const float *x, int N, int C, int H, int W, const float *w, 
     return 0;
 }
 
+/*
+ * Bilinear resize of NCHW planes from Hin x Win to H x W (the "Resize" step of
+ * the paper's Resize-Conv-ReLU-Maxpool block, "Evaluation"; the paper does not
+ * give the interpolation mode, this reads it as bilinear with half-pixel
+ * centres). Output pixel (y, x) samples the input at
+ *   sy = (y + 1/2) * Hin / H - 1/2,   sx = (x + 1/2) * Win / W - 1/2,
+ * clamped below at 0; with i0 = floor(s), i1 = min(i0 + 1, in - 1) and
+ * t = s - i0 per axis, the value is
+ *   (1-ty) * ((1-tx) v[i0y][i0x] + tx v[i0y][i1x]) + ty * ((1-tx) v[i1y][i0x] + tx v[i1y][i1x]).
+ * The coordinates are taken as exact fractions (numerator (2y+1)*Hin - H over
+ * 2H), the arithmetic in double. absout receives the sum of |weight * value|
+ * of the four terms, which bounds the rounding of an fp32 evaluation.
+ */
+void oracle_resize_bilinear(const float *x, int N, int C, int Hin, int Win, int H, int W, double *out,
+                            double *absout) {
+    for (long long pl = 0; pl < (long long)N * C; ++pl) {
+        const float *src = x + pl * Hin * Win;
+        for (int y = 0; y < H; ++y) {
+            long long ny = (2LL * y + 1) * Hin - H;   /* sy = ny / (2H) */
+            if (ny < 0) ny = 0;
+            const long long y0 = ny / (2LL * H);
+            const long long y1 = y0 + 1 < Hin ? y0 + 1 : Hin - 1;
+            const double ty = (double)(ny - y0 * 2LL * H) / (2.0 * H);
+            for (int xo = 0; xo < W; ++xo) {
+                long long nx = (2LL * xo + 1) * Win - W;
+                if (nx < 0) nx = 0;
+                const long long x0 = nx / (2LL * W);
+                const long long x1 = x0 + 1 < Win ? x0 + 1 : Win - 1;
+                const double tx = (double)(nx - x0 * 2LL * W) / (2.0 * W);
+                const double v00 = src[y0 * Win + x0], v01 = src[y0 * Win + x1];
+                const double v10 = src[y1 * Win + x0], v11 = src[y1 * Win + x1];
+                const double w00 = (1 - ty) * (1 - tx), w01 = (1 - ty) * tx, w10 = ty * (1 - tx), w11 = ty * tx;
+                const size_t o = (size_t)pl * H * W + (size_t)y * W + xo;
+                out[o] = w00 * v00 + w01 * v01 + w10 * v10 + w11 * v11;
+                absout[o] = fabs(w00 * v00) + fabs(w01 * v01) + fabs(w10 * v10) + fabs(w11 * v11);
+            }
+        }
+    }
+}
+
 /* oracle_conv_res without a residual. */
 int oracle_conv(const float *x, int N, int C, int H, int W, const float *w, const uint8_t *mask, int K, int R,
                 int S, const float *bias, int stride, int pad, int relu, int pool, const int32_t *pairs,

@@ -341,6 +341,45 @@ def pin_residual_closed_forms(orc):
     assert np.array_equal(gp, wp)
 
 
+def _torch_resize(x, H, W):
+    X = torch.from_numpy(np.asarray(x, np.float64))
+    return F.interpolate(X, size=(H, W), mode="bilinear", align_corners=False).numpy()
+
+
+def pin_resize_library(orc):
+    """Bilinear resize (half-pixel centres) == float64
+    torch.nn.functional.interpolate(mode="bilinear", align_corners=False) on
+    random shapes: up, down, non-integer ratios, H != W, one-pixel planes; and
+    its sum of |w*v| == the same interpolation of |x| (the weights are >= 0)."""
+    rng = _rng(41)
+    for _ in range(40):
+        N, C = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+        Hin, Win = int(rng.integers(1, 12)), int(rng.integers(1, 12))
+        H, W = int(rng.integers(1, 25)), int(rng.integers(1, 25))
+        x = rng.uniform(-1, 1, (N, C, Hin, Win)).astype(np.float32)
+        got, ab = orc.resize(x, H, W)
+        ref = _torch_resize(x, H, W)
+        assert np.allclose(got, ref, rtol=0, atol=1e-12), float(np.abs(got - ref).max())
+        assert np.allclose(ab, _torch_resize(np.abs(x), H, W), rtol=0, atol=1e-12)
+
+
+def pin_resize_closed_forms(orc):
+    """Same size: an exact copy. Exact factor-2 downsampling: the mean of each
+    2x2 block. A constant plane stays constant at any size (the four weights
+    sum to one up to double rounding)."""
+    rng = _rng(42)
+    x = rng.uniform(-1, 1, (2, 3, 6, 10)).astype(np.float32)
+    got, _ = orc.resize(x, 6, 10)
+    assert np.array_equal(got, x.astype(np.float64))
+    got, _ = orc.resize(x, 3, 5)
+    ref = x.astype(np.float64).reshape(2, 3, 3, 2, 5, 2).mean(axis=(3, 5))
+    assert np.allclose(got, ref, rtol=0, atol=1e-15)
+    c = np.full((1, 2, 5, 7), 0.75, np.float32)
+    for H, W in ((1, 1), (9, 3), (10, 14), (4, 4)):
+        got, _ = orc.resize(c, H, W)
+        assert np.allclose(got, 0.75, rtol=0, atol=1e-15)
+
+
 ALL_PINS = [
     pin_library_conv,
     pin_library_absacc,
@@ -356,4 +395,6 @@ ALL_PINS = [
     pin_csr_golden,
     pin_library_residual,
     pin_residual_closed_forms,
+    pin_resize_library,
+    pin_resize_closed_forms,
 ]

@@ -37,6 +37,12 @@ MUTANTS = {
     "residual_after_relu": ("    if (res) {\n        const float *rp", "    if (relu)\n        for (int i = 0; i < Ho * Wo; ++i) acc[i] = acc[i] > 0.0 ? acc[i] : 0.0;\n    if (res) {\n        const float *rp"),
     "residual_batch_ignored": ("const float *rp = res + ((size_t)n * K + k) * Ho * Wo;", "const float *rp = res + ((size_t)k) * Ho * Wo;"),
     "residual_sign": ("acc[i] += (double)rp[i];", "acc[i] -= (double)rp[i];"),
+    "resize_no_half_pixel": ("long long ny = (2LL * y + 1) * Hin - H;", "long long ny = 2LL * y * Hin;"),
+    "resize_no_clamp": ("            if (ny < 0) ny = 0;\n", "\n"),
+    "resize_weights_swapped": ("const double w00 = (1 - ty) * (1 - tx), w01 = (1 - ty) * tx,",
+                               "const double w00 = (1 - ty) * tx, w01 = (1 - ty) * (1 - tx),"),
+    "resize_x_fraction_from_height": ("const double tx = (double)(nx - x0 * 2LL * W) / (2.0 * W);",
+                                      "const double tx = (double)(nx - x0 * 2LL * W) / (2.0 * H);"),
     "pack_last_row_dropped": ("for (int k = 0; k < K; ++k) {\n        for (int c = 0; c < C; ++c)\n            for (int r = 0; r < R; ++r)\n                for (int s = 0; s < S; ++s) {\n                    size_t i",
                               "for (int k = 0; k < K - 1; ++k) {\n        for (int c = 0; c < C; ++c)\n            for (int r = 0; r < R; ++r)\n                for (int s = 0; s < S; ++s) {\n                    size_t i"),
 }
