@@ -39,7 +39,23 @@ BLOCKS = {
                  "bias+ReLU, the second with 2x2 max-pool; fp32",
     "resnet_block": "ResNet basic block: N=32, C=K=64, 56x56, relu(conv2(relu(conv1(x))) + x), 3x3 convs, "
                     "density 0.2, bias; fp32",
+    "resize_block": "Resize-Conv-ReLU-Maxpool: N=32, C=K=128, bilinear resize 42x42 -> 28x28 (pixel centres "
+                    "aligned), 3x3 conv density 0.1, bias+ReLU+2x2 max-pool to 14x14; fp32",
 }
+
+
+def resize_source_bytes(planes, Hin, Win, H, W):
+    """Bytes of the source a bilinear resize must read: the source rows and
+    columns that some output pixel takes a tap from (all of them unless the
+    downscale exceeds 2x), once each."""
+    def taps(n_in, n_out):
+        used = set()
+        for o in range(n_out):
+            num = max((2 * o + 1) * n_in - n_out, 0)
+            i0 = num // (2 * n_out)
+            used.update((i0, min(i0 + 1, n_in - 1)))
+        return len(used)
+    return 4.0 * planes * taps(Hin, H) * taps(Win, W)
 
 
 def algorithmic(layer, nnz):
@@ -148,6 +164,8 @@ def bench_block(args, dev):
 
     from paper_2005_04091_amd import spconv, synth
 
+    if args.workload == "resize_block":
+        return bench_resize_block(args, dev)
     x, l1, l2 = synth.make_vgg_block() if args.workload == "vgg_block" else synth.make_resnet_block()
     resnet = args.workload == "resnet_block"
     N, C, H, W, K, R, S = l1.shape
@@ -205,6 +223,83 @@ def bench_block(args, dev):
                    "nnz": [nnz1, nnz2], "pool": bool(l2.pool), "residual": resnet},
         "ms_per_step_unfused": round(ms_unfused, 5),
         "fusion_saving_frac": round(1.0 - ms / ms_unfused, 4),
+    }
+    print(json.dumps(rec), flush=True)
+
+
+def _timed(args, stream, step):
+    import torch
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / args.steps
+
+
+def bench_resize_block(args, dev):
+    """Resize-Conv-ReLU-Maxpool per step, source resident in HBM: the resize
+    writes the conv's padded input directly (one pass), then the fused conv +
+    bias + ReLU + max-pool. `unfused` resizes into a plain tensor and pads it
+    in a second pass before the same conv. The resize kernel is also timed on
+    its own, against its algorithmic bytes (source taps read once, padded
+    output written once)."""
+    import torch
+
+    from paper_2005_04091_amd import spconv, synth
+
+    src, layer = synth.make_resize_block()
+    N, C, H, W, K, R, S = layer.shape
+    Hin, Win = int(src.shape[2]), int(src.shape[3])
+    L = spconv.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, 1, 1, True, True, device=dev)
+    sd = torch.from_numpy(src).to(dev)
+    xr = torch.empty((N, C, H, W), dtype=torch.float32, device=dev)
+    xp = torch.empty((N, C, H + 2, W + 2), dtype=torch.float32, device=dev)
+    y = torch.empty((N, K, L.Ho, L.Wo), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fused():
+        L.resize_pad_input(sd, out=xp, stream=stream)
+        L.forward_padded(xp, out=y, stream=stream)
+
+    def unfused():
+        spconv.spconv_resize_pad_input(sd, H, W, 0, out=xr, stream=stream)
+        L.pad_input(xr, out=xp, stream=stream)
+        L.forward_padded(xp, out=y, stream=stream)
+
+    def resize_only():
+        L.resize_pad_input(sd, out=xp, stream=stream)
+
+    ms = _timed(args, stream, fused)
+    ms_unfused = _timed(args, stream, unfused)
+    ms_resize = _timed(args, stream, resize_only)
+    nnz = L.host_csr.nnz
+    flops = 2.0 * nnz * N * H * W
+    rbytes = resize_source_bytes(N * C, Hin, Win, H, W) + 4.0 * N * C * (H + 2) * (W + 2)
+    rec = {
+        "metric": "ms/layer + nonzero GFLOP/s + % HBM roofline, fused sparse conv, 1 MI355X",
+        "value": round(flops / (ms * 1e-3) / 1e9, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded Bernoulli-masked weights U[-1,1), source U[0,1), bias U[-0.1,0.1))",
+        "config": {"workload": BLOCKS[args.workload], "N": N, "C": C, "K": K, "Hin": Hin, "Win": Win, "H": H,
+                   "W": W, "nnz": nnz, "pool": True},
+        "ms_per_step_unfused": round(ms_unfused, 5),
+        "fusion_saving_frac": round(1.0 - ms / ms_unfused, 4),
+        "resize_kernel": {"ms": round(ms_resize, 5), "algorithmic_bytes": rbytes,
+                          "GB/s": round(rbytes / (ms_resize * 1e-3) / 1e9, 1),
+                          "hbm_frac": round(rbytes / (ms_resize * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
     }
     print(json.dumps(rec), flush=True)
 

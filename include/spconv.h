@@ -98,10 +98,38 @@ int spconv_pack_csr(const float *w, const uint8_t *mask, int K, int C, int R, in
  * in          [N][C][H][W] fp32, device.
  * out_padded  [N][C][H+2pad][W+2pad] fp32, device, must not overlap `in`.
  * stream      HIP stream the copy is queued on (0 = the null stream).
- * Errors: SPCONV_EINVAL (NULL pointer, N/C/H/W < 1, pad < 0, element count
- * >= 2^40); SPCONV_EHIP when the launch fails.
+ * Errors: SPCONV_EINVAL (NULL pointer, N/C/H/W < 1, pad < 0, a padded plane
+ * of 2^31 - 4096 elements or more, element count >= 2^40); SPCONV_EHIP when the
+ * launch fails.
  */
 int spconv_pad_input(const float *in, int N, int C, int H, int W, int pad, float *out_padded, hipStream_t stream);
+
+/*
+ * spconv_resize_pad_input - bilinear resize of an NCHW tensor written straight
+ * into the zero-padded layout spconv_forward reads (device, asynchronous).
+ *
+ * The resize step that precedes the convolution in the Resize-Conv-ReLU-Maxpool
+ * block of the paper's evaluation (Evaluation, deep learning benchmarks), done in
+ * the same pass as the padding so the block needs no separate pad pass. The
+ * paper does not name the interpolation; this is bilinear with pixel centres
+ * aligned (align_corners = false): output pixel (y, x) samples the input at
+ *   sy = max((y + 1/2) * Hin / H - 1/2, 0),  sx = max((x + 1/2) * Win / W - 1/2, 0)
+ * from taps y0 = floor(sy), y1 = min(y0 + 1, Hin - 1) (x likewise) with weights
+ * (1 - ty, ty), ty = sy - y0:
+ *   out_padded[n][c][y+pad][x+pad] = sum over the 2x2 taps of weight * in[n][c][yi][xi],
+ *   border = +0.0.
+ * Coordinates are exact integer ratios; the interpolation is fp32 in the form
+ * a + t*(b - a), so an axis whose size does not change is copied exactly
+ * (H == Hin and W == Win reproduce spconv_pad_input bit for bit).
+ * in          [N][C][Hin][Win] fp32, device.
+ * out_padded  [N][C][H+2pad][W+2pad] fp32, device, must not overlap `in`.
+ * stream      HIP stream the pass is queued on (0 = the null stream).
+ * Errors: SPCONV_EINVAL (NULL pointer, N/C/Hin/Win/H/W < 1, pad < 0, a side
+ * above 16384, a padded plane of 2^31 elements or more, input or output
+ * element count >= 2^40); SPCONV_EHIP when the launch fails.
+ */
+int spconv_resize_pad_input(const float *in, int N, int C, int Hin, int Win, int H, int W, int pad,
+                            float *out_padded, hipStream_t stream);
 
 /*
  * spconv_forward - fused sparse convolution + bias + ReLU + 2x2 max-pool

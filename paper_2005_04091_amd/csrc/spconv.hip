@@ -57,35 +57,54 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shi
 // Padded input (spconv_pad_input)
 // ---------------------------------------------------------------------------
 
+// Streaming stores (nontemporal): the padded tensors are written once, by
+// whole cache lines, and read back by the next kernel; on gfx950 such stores
+// sustain a markedly higher write rate than ordinary ones.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void stream_store(float *p, float v) { __builtin_nontemporal_store(v, p); }
+
+__device__ __forceinline__ void stream_store4(float *p, float4 v) {
+    const f32x4_t t = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(t, reinterpret_cast<f32x4_t *>(p));
+}
+
 // The padded tensor is treated as one flat array of 4-element quads. A
 // workgroup covers kPadQuads consecutive quads per thread: in round j thread t
 // writes quad (block*kPadQuads + j)*256 + t with one 16-byte store (when the
 // output is 16-byte aligned), so each round's stores coalesce; a quad inside
 // one input row is fetched with one 16-byte load, border quads element by
 // element (0 outside the input). All loads of a thread are issued before its
-// stores.
+// stores. The workgroup's first plane takes one 64-bit division; every quad's
+// plane, row and column inside the workgroup's span take 32-bit
+// multiply-shift divisions.
 constexpr int kPadQuads = 4;
+constexpr int kPadSpan = 4 * kThreads * kPadQuads;  // elements per workgroup
 
 struct PadArgs {
     const float *in;
     float *out;
-    long long total;      // N*C*Hp*Wp
+    long long total;       // N*C*Hp*Wp
     int H, W, pad, Hp, Wp;
-    int plane;            // Hp*Wp
-    uint32_t wp_magic;    // x / Wp == (x * wp_magic) >> wp_shift for 0 <= x < 2^31
+    int plane;             // Hp*Wp, at most 2^31 - 1 - kPadSpan
+    uint32_t plane_magic;  // x / plane == (x * plane_magic) >> plane_shift for 0 <= x < 2^31
+    int plane_shift;
+    uint32_t wp_magic;     // x / Wp likewise
     int wp_shift;
 };
 
-__device__ __forceinline__ float4 pad_quad(const PadArgs &a, long long f0) {
-    long long pid = f0 / a.plane;  // plane (n, c) of the first element
-    const int e = (int)(f0 - pid * a.plane);
+// Quad starting at flat element f0 = pbase*plane + e (0 <= e < plane + kPadSpan).
+__device__ __forceinline__ float4 pad_quad(const PadArgs &a, long long f0, long long pbase, int e) {
+    const int q = (int)fast_div((uint32_t)e, a.plane_magic, a.plane_shift);
+    long long pid = pbase + q;  // plane (n, c) of the first element
+    e -= q * a.plane;
     int yp = (int)fast_div((uint32_t)e, a.wp_magic, a.wp_shift);
     int xp = e - yp * a.Wp;
     const int y0 = yp - a.pad, x0 = xp - a.pad;
     if (f0 + 3 < a.total && y0 >= 0 && y0 < a.H && x0 >= 0 && x0 + 3 < a.W) {
-        float4 q;  // all four inside one input row: one 16-byte load (4-byte aligned)
-        __builtin_memcpy(&q, a.in + pid * a.H * a.W + (long long)y0 * a.W + x0, sizeof(q));
-        return q;
+        float4 v;  // all four inside one input row: one 16-byte load (4-byte aligned)
+        __builtin_memcpy(&v, a.in + pid * a.H * a.W + (long long)y0 * a.W + x0, sizeof(v));
+        return v;
     }
     float v[4];
 #pragma unroll
@@ -107,24 +126,189 @@ __device__ __forceinline__ float4 pad_quad(const PadArgs &a, long long f0) {
 
 template <bool VEC>
 __global__ __launch_bounds__(kThreads) void pad_nchw_kernel(PadArgs a) {
+    const long long fb = (long long)blockIdx.x * kPadSpan;
+    const long long pbase = fb / a.plane;
+    const int eb = (int)(fb - pbase * a.plane);
     float4 q[kPadQuads];
-    long long f[kPadQuads];
 #pragma unroll
     for (int j = 0; j < kPadQuads; ++j) {
-        f[j] = (((long long)blockIdx.x * kPadQuads + j) * kThreads + threadIdx.x) * 4;
-        if (f[j] < a.total) q[j] = pad_quad(a, f[j]);
+        const int off = (j * kThreads + (int)threadIdx.x) * 4;
+        if (fb + off < a.total) q[j] = pad_quad(a, fb + off, pbase, eb + off);
     }
 #pragma unroll
     for (int j = 0; j < kPadQuads; ++j) {
-        if (f[j] >= a.total) break;
-        if (VEC && f[j] + 3 < a.total) {
-            *reinterpret_cast<float4 *>(a.out + f[j]) = q[j];
+        const long long f = fb + (j * kThreads + (int)threadIdx.x) * 4;
+        if (f >= a.total) break;
+        if (VEC && f + 3 < a.total) {
+            stream_store4(a.out + f, q[j]);
         } else {
             const float v[4] = {q[j].x, q[j].y, q[j].z, q[j].w};
 #pragma unroll
             for (int u = 0; u < 4; ++u)
-                if (f[j] + u < a.total) a.out[f[j] + u] = v[u];
+                if (f + u < a.total) stream_store(a.out + f + u, v[u]);
         }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Bilinear resize into the padded layout (spconv_resize_pad_input)
+// ---------------------------------------------------------------------------
+
+// Output coordinate o of an axis resized from n_in to n_out samples the input
+// at s = (o + 1/2) * n_in / n_out - 1/2 (pixel centres aligned), clamped below
+// at 0, between the taps i0 = floor(s) and i1 = min(i0 + 1, n_in - 1), with
+// weight t = s - i0 on i1. In integers s = num / (2 n_out) with
+// num = (2o + 1) n_in - n_out, so i0 is exact and t is the correctly rounded
+// float of an exact fraction. Sides are at most 16384, so num < 2^30.
+struct ResizeTap {
+    int i0, i1;
+    float t;
+};
+
+__device__ __forceinline__ ResizeTap resize_tap(int o, int n_in, int n_out) {
+    const int num = max((2 * o + 1) * n_in - n_out, 0);
+    const int den = 2 * n_out;
+    ResizeTap r;
+    r.i0 = num / den;
+    r.i1 = min(r.i0 + 1, n_in - 1);
+    r.t = (float)(num - r.i0 * den) / (float)den;
+    return r;
+}
+
+// Interpolation in lerp form: with t = 0 (an axis of unchanged size) it
+// returns its first operand exactly, so an unchanged plane is copied bitwise.
+__device__ __forceinline__ float lerp_f(float a, float b, float t) { return a + t * (b - a); }
+
+struct ResizeArgs {
+    int Hin, Win, H, W, pad, Hp, Wp;
+    int bands;       // row bands per plane, one workgroup each
+    int band_rows;   // padded output rows per band
+};
+
+constexpr int kResizeMaxSide = 16384;
+constexpr int kResizeTargetWgs = 2048;  // split planes into row bands until the grid has this many workgroups
+
+// Row variant, for planes too large for the flat variant's LDS tables (any
+// width): one workgroup writes one band of padded rows of one (n, c) plane;
+// waves take the band's rows round-robin and each row is written 64 columns at
+// a time (coalesced stores; the two source rows of a row are read by one
+// wave). Border rows and columns are written as +0.0.
+__global__ __launch_bounds__(kThreads) void resize_pad_rows_kernel(ResizeArgs a, const float *__restrict__ in,
+                                                                   float *__restrict__ out) {
+    const int lane = (int)threadIdx.x & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x / kWave);
+    const int plane = (int)blockIdx.x / a.bands;
+    const int band = (int)blockIdx.x - plane * a.bands;
+    const float *src = in + (size_t)plane * a.Hin * a.Win;
+    float *dst = out + (size_t)plane * a.Hp * a.Wp;
+    const int r1 = min(a.Hp, (band + 1) * a.band_rows);
+    for (int yp = band * a.band_rows + wave; yp < r1; yp += kWaves) {
+        float *drow = dst + (size_t)yp * a.Wp;
+        const int y = yp - a.pad;
+        if (y < 0 || y >= a.H) {  // a border row (wave-uniform)
+            for (int xp = lane; xp < a.Wp; xp += kWave) stream_store(drow + xp, 0.0f);
+            continue;
+        }
+        const ResizeTap ty = resize_tap(y, a.Hin, a.H);
+        const float *s0 = src + (size_t)ty.i0 * a.Win;
+        const float *s1 = src + (size_t)ty.i1 * a.Win;
+        for (int xp = lane; xp < a.Wp; xp += kWave) {
+            const int x = xp - a.pad;
+            float o = 0.0f;
+            if (x >= 0 && x < a.W) {
+                const ResizeTap t = resize_tap(x, a.Win, a.W);
+                o = lerp_f(lerp_f(s0[t.i0], s0[t.i1], t.t), lerp_f(s1[t.i0], s1[t.i1], t.t), ty.t);
+            }
+            stream_store(drow + xp, o);
+        }
+    }
+}
+
+// Flat variant for planes whose two tap tables fit in LDS (Hp + Wp entries):
+// the padded output of all planes is one flat array, each thread takes
+// kResizeFlatElems elements 256 apart (every lane busy whatever the width, each
+// round one coalesced store per wave) and issues the loads of all of them
+// before the first store. Per element: (plane, row, column) by multiply-shift
+// division, the row and column taps from the tables, four loads at 32-bit
+// offsets from the workgroup's first plane, three interpolations.
+constexpr int kResizeFlatElems = 8;
+constexpr int kResizeFlatMaxTab = 4096;   // Hp + Wp; 12 B of LDS per entry
+
+struct ResizeFlatArgs {
+    int Hin, Win, H, W, pad, Hp, Wp;
+    int ps;               // Hp * Wp
+    uint32_t ps_magic;    // x / ps == (x * ps_magic) >> ps_shift for 0 <= x < 2^31
+    int ps_shift;
+    uint32_t wp_magic;    // x / Wp likewise
+    int wp_shift;
+    long long total;      // planes * ps
+};
+
+__global__ __launch_bounds__(kThreads) void resize_pad_flat_kernel(ResizeFlatArgs a, const float *__restrict__ in,
+                                                                   float *__restrict__ out) {
+    // Tables, entry i < Hp for padded row i, Hp + x for padded column x:
+    // first and second tap (row taps pre-multiplied by Win; -1 = border) and
+    // the weight of the second.
+    extern __shared__ int tab[];
+    const int nt = a.Hp + a.Wp;
+    int *tap0 = tab;
+    int *tap1 = tab + nt;
+    float *tapw = reinterpret_cast<float *>(tab + 2 * nt);
+    for (int i = (int)threadIdx.x; i < nt; i += kThreads) {
+        const bool row = i < a.Hp;
+        const int o = (row ? i : i - a.Hp) - a.pad;
+        const int n_out = row ? a.H : a.W;
+        const int scale = row ? a.Win : 1;
+        int t0 = -1, t1 = 0;
+        float w = 0.0f;
+        if (o >= 0 && o < n_out) {
+            const ResizeTap r = resize_tap(o, row ? a.Hin : a.Win, n_out);
+            t0 = r.i0 * scale;
+            t1 = r.i1 * scale;
+            w = r.t;
+        }
+        tap0[i] = t0;
+        tap1[i] = t1;
+        tapw[i] = w;
+    }
+    __syncthreads();
+
+    constexpr int E = kResizeFlatElems;
+    const long long f0 = (long long)blockIdx.x * (kThreads * E);
+    const long long p0 = f0 / a.ps;
+    const int e0 = (int)(f0 - p0 * a.ps);
+    const float *sblk = in + p0 * a.Hin * a.Win;  // the workgroup's first source plane
+    const uint32_t src_plane = (uint32_t)(a.Hin * a.Win);
+    float v[E][4];
+    float tx[E], ty[E];
+    bool inside[E];
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        const int e = e0 + j * kThreads + (int)threadIdx.x;
+        const uint32_t q = fast_div((uint32_t)e, a.ps_magic, a.ps_shift);
+        const int ee = e - (int)q * a.ps;
+        const int yp = (int)fast_div((uint32_t)ee, a.wp_magic, a.wp_shift);
+        const int xp = ee - yp * a.Wp;
+        const int r0 = tap0[yp], c0 = tap0[a.Hp + xp];
+        inside[j] = f0 + j * kThreads + threadIdx.x < a.total && (r0 | c0) >= 0;
+        ty[j] = tapw[yp];
+        tx[j] = tapw[a.Hp + xp];
+        if (inside[j]) {
+            const int r1 = tap1[yp], c1 = tap1[a.Hp + xp];
+            const uint32_t pb = q * src_plane;
+            v[j][0] = sblk[pb + (uint32_t)(r0 + c0)];
+            v[j][1] = sblk[pb + (uint32_t)(r0 + c1)];
+            v[j][2] = sblk[pb + (uint32_t)(r1 + c0)];
+            v[j][3] = sblk[pb + (uint32_t)(r1 + c1)];
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+        const long long f = f0 + j * kThreads + threadIdx.x;
+        if (f >= a.total) break;
+        float o = 0.0f;
+        if (inside[j]) o = lerp_f(lerp_f(v[j][0], v[j][1], tx[j]), lerp_f(v[j][2], v[j][3], tx[j]), ty[j]);
+        stream_store(out + f, o);
     }
 }
 
@@ -1138,7 +1322,7 @@ extern "C" int spconv_pad_input(const float *in, int N, int C, int H, int W, int
     const long long Hp = (long long)H + 2LL * pad, Wp = (long long)W + 2LL * pad;
     const long long plane = Hp * Wp;
     const long long planes = (long long)N * C;
-    if (plane >= (1LL << 31) || planes * plane >= (1LL << 40)) return SPCONV_EINVAL;
+    if (plane >= (1LL << 31) - kPadSpan || planes * plane >= (1LL << 40)) return SPCONV_EINVAL;
     PadArgs a;
     a.in = in;
     a.out = out_padded;
@@ -1149,13 +1333,70 @@ extern "C" int spconv_pad_input(const float *in, int N, int C, int H, int W, int
     a.Hp = (int)Hp;
     a.Wp = (int)Wp;
     a.plane = (int)plane;
-    if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift)) return SPCONV_EINVAL;
-    const long long per_block = 4LL * kThreads * kPadQuads;
+    if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift) ||
+        !div_magic((uint32_t)plane, &a.plane_magic, &a.plane_shift))
+        return SPCONV_EINVAL;
+    const long long per_block = kPadSpan;
     const long long blocks = (a.total + per_block - 1) / per_block;
     if (blocks > 0x7fffffffLL) return SPCONV_EINVAL;
     const bool vec = (reinterpret_cast<uintptr_t>(out_padded) & 15) == 0;
     hipLaunchKernelGGL(vec ? pad_nchw_kernel<true> : pad_nchw_kernel<false>, dim3((unsigned)blocks), dim3(kThreads),
                        0, stream, a);
+    return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+}
+
+extern "C" int spconv_resize_pad_input(const float *in, int N, int C, int Hin, int Win, int H, int W, int pad,
+                                       float *out_padded, hipStream_t stream) {
+    if (!in || !out_padded || N < 1 || C < 1 || Hin < 1 || Win < 1 || H < 1 || W < 1 || pad < 0)
+        return SPCONV_EINVAL;
+    if (Hin > kResizeMaxSide || Win > kResizeMaxSide || H > kResizeMaxSide || W > kResizeMaxSide)
+        return SPCONV_EINVAL;
+    const long long Hp = (long long)H + 2LL * pad, Wp = (long long)W + 2LL * pad;
+    const long long planes = (long long)N * C;
+    if (Hp * Wp >= (1LL << 31) || planes * Hp * Wp >= (1LL << 40) || planes * Hin * Win >= (1LL << 40))
+        return SPCONV_EINVAL;
+    // Flat kernel when both tap tables fit in LDS and the source planes one
+    // workgroup can touch are addressable with 32-bit offsets (in elements).
+    const long long ps = Hp * Wp;
+    const long long span_planes = (long long)kThreads * kResizeFlatElems / ps + 2;
+    if (Hp + Wp <= kResizeFlatMaxTab && span_planes * Hin * Win < (1LL << 31)) {
+        ResizeFlatArgs f;
+        f.Hin = Hin;
+        f.Win = Win;
+        f.H = H;
+        f.W = W;
+        f.pad = pad;
+        f.Hp = (int)Hp;
+        f.Wp = (int)Wp;
+        f.ps = (int)ps;
+        f.total = planes * ps;
+        if (!div_magic((uint32_t)ps, &f.ps_magic, &f.ps_shift) || !div_magic((uint32_t)Wp, &f.wp_magic, &f.wp_shift))
+            return SPCONV_EINVAL;
+        const long long per_block = (long long)kThreads * kResizeFlatElems;
+        const long long blocks = (f.total + per_block - 1) / per_block;
+        if (blocks > 0x7fffffffLL) return SPCONV_EINVAL;
+        const size_t lds = (size_t)(Hp + Wp) * 3 * sizeof(int);
+        hipLaunchKernelGGL(resize_pad_flat_kernel, dim3((unsigned)blocks), dim3(kThreads), lds, stream, f, in,
+                           out_padded);
+        return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+    }
+    ResizeArgs a;
+    a.Hin = Hin;
+    a.Win = Win;
+    a.H = H;
+    a.W = W;
+    a.pad = pad;
+    a.Hp = (int)Hp;
+    a.Wp = (int)Wp;
+    const long long max_bands = (Hp + kWaves - 1) / kWaves;
+    const long long want = (kResizeTargetWgs + planes - 1) / planes;
+    const long long bands0 = std::max(1LL, std::min(want, max_bands));
+    a.band_rows = (int)((Hp + bands0 - 1) / bands0);
+    a.bands = (int)((Hp + a.band_rows - 1) / a.band_rows);
+    const long long blocks = planes * a.bands;
+    if (blocks > 0x7fffffffLL) return SPCONV_EINVAL;
+    hipLaunchKernelGGL(resize_pad_rows_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, a, in,
+                       out_padded);
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 

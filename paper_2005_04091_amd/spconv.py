@@ -24,7 +24,7 @@ SPCONV_EHIP = -3
 SPCONV_RELU = 1
 SPCONV_MAXPOOL2X2 = 2
 
-EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
+EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
             "spconv_output_shape", "spconv_strerror")
 SPCONV_KERNEL_STRIDE1 = 1
 SPCONV_KERNEL_GENERIC = 2
@@ -63,6 +63,8 @@ def _bind(lib):
                                     ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
     lib.spconv_pad_input.restype = _c_int
     lib.spconv_pad_input.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, _c_int, _vp, _vp]
+    lib.spconv_resize_pad_input.restype = _c_int
+    lib.spconv_resize_pad_input.argtypes = [_vp] + [_c_int] * 7 + [_vp, _vp]
     lib.spconv_forward.restype = _c_int
     lib.spconv_forward.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int,
                                    _c_int, _c_int, _c_int, _vp, ctypes.c_uint32, _vp, _vp]
@@ -181,6 +183,17 @@ def _dev_ptr(t, name):
     return t.data_ptr()
 
 
+def _check_shape(t, shape, name):
+    if tuple(int(v) for v in t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _check_numel(t, n, name):
+    """The kernels index raw pointers: a buffer must hold every element they touch."""
+    if t is not None and t.numel() < n:
+        raise ValueError(f"{name} holds {t.numel()} elements, the call needs {n}")
+
+
 def _stream_handle(stream, device):
     import torch
     s = stream if stream is not None else torch.cuda.current_stream(device)
@@ -195,8 +208,26 @@ def spconv_pad_input(x, pad: int, out=None, stream=None):
     N, C, H, W = (int(v) for v in x.shape)
     if out is None:
         out = torch.empty((N, C, H + 2 * pad, W + 2 * pad), dtype=torch.float32, device=x.device)
+    _check_shape(out, (N, C, H + 2 * pad, W + 2 * pad), "out")
     _check(_lib.spconv_pad_input(_dev_ptr(x, "x"), N, C, H, W, pad, _dev_ptr(out, "out"),
                                  _stream_handle(stream, x.device)), "spconv_pad_input")
+    return out
+
+
+def spconv_resize_pad_input(x, H: int, W: int, pad: int, out=None, stream=None):
+    """Bilinear resize (pixel centres aligned) of NCHW ``x`` to H x W, written
+    with a zero border of ``pad`` into ``out`` [N, C, H+2pad, W+2pad] (device),
+    queued on ``stream``."""
+    import torch
+    if x.dim() != 4:
+        raise ValueError("x must be NCHW")
+    N, C, Hin, Win = (int(v) for v in x.shape)
+    shape = (N, C, H + 2 * pad, W + 2 * pad)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=x.device)
+    _check_shape(out, shape, "out")
+    _check(_lib.spconv_resize_pad_input(_dev_ptr(x, "x"), N, C, Hin, Win, H, W, pad, _dev_ptr(out, "out"),
+                                        _stream_handle(stream, x.device)), "spconv_resize_pad_input")
     return out
 
 
@@ -207,6 +238,9 @@ def spconv_forward(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R
     Ho, Wo = spconv_output_shape(H, W, R, S, stride, pad, flags)
     if out is None:
         out = torch.empty((N, K, Ho, Wo), dtype=torch.float32, device=xp.device)
+    _check_numel(xp, N * C * (H + 2 * pad) * (W + 2 * pad), "xp")
+    _check_numel(out, N * K * Ho * Wo, "out")
+    _check_numel(bias, K, "bias")
     _check(_lib.spconv_forward(_dev_ptr(xp, "xp"), N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad,
                                _dev_ptr(bias, "bias"), flags, _dev_ptr(out, "out"),
                                _stream_handle(stream, xp.device)), "spconv_forward")
@@ -224,6 +258,11 @@ def spconv_forward_ex(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int
     Hs, Ws = spconv_output_shape(H, W, R, S, stride, pad, flags)
     if out is None:
         out = torch.empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), dtype=torch.float32, device=xp.device)
+    Hc, Wc = spconv_output_shape(H, W, R, S, stride, pad, flags & ~SPCONV_MAXPOOL2X2)
+    _check_numel(xp, N * C * (H + 2 * pad) * (W + 2 * pad), "xp")
+    _check_numel(out, N * K * (Hs + 2 * out_pad) * (Ws + 2 * out_pad), "out")
+    _check_numel(bias, K, "bias")
+    _check_numel(residual, N * K * (Hc + 2 * residual_pad) * (Wc + 2 * residual_pad), "residual")
     epi = spconv_epilogue(out_pad, residual_pad, _dev_ptr(residual, "residual"))
     _check(_lib.spconv_forward_ex(_dev_ptr(xp, "xp"), N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad,
                                   _dev_ptr(bias, "bias"), flags, ctypes.byref(epi), _dev_ptr(out, "out"),
@@ -265,6 +304,10 @@ class SparseConvLayer:
 
     def pad_input(self, x, out=None, stream=None):
         return spconv_pad_input(x, self.pad, out=out, stream=stream)
+
+    def resize_pad_input(self, x, out=None, stream=None):
+        """Bilinear resize of ``x`` to this layer's H x W, written as its padded input."""
+        return spconv_resize_pad_input(x, self.H, self.W, self.pad, out=out, stream=stream)
 
     def forward_padded(self, xp, out=None, stream=None, out_pad: int = 0, residual=None, residual_pad: int = 0):
         """Fused forward on the padded input. With ``out_pad`` the output planes

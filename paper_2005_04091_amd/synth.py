@@ -153,6 +153,29 @@ def make_resnet_block():
     return x, l1, l2
 
 
+# Resize-Conv-ReLU-Maxpool: the Conv-ReLU-Maxpool layer (28x28, C=K=128, density
+# 0.1, pool to 14x14) fed by a bilinear resize of a 42x42 source (a 1.5x
+# downscale, so every output pixel interpolates between two source pixels on
+# each axis, at fractions 1/4 and 3/4).
+RESIZE_BLOCK = dict(N=32, C=128, K=128, Hin=42, Win=42, H=28, W=28, density=0.1, seed=SEED_BASE + 7)
+
+
+def make_resize_block():
+    """Source image batch and the layer of the Resize-Conv-ReLU-Maxpool block.
+    Draw order: mask, weights, source, bias. Returns ``(src, layer)``; the
+    layer's ``x`` is a seeded U[0, 1) tensor of its own input shape (for the
+    layer alone; in the block it reads the resized source)."""
+    cfg = RESIZE_BLOCK
+    rng = np.random.default_rng(cfg["seed"])
+    N, C, K, H, W, d = cfg["N"], cfg["C"], cfg["K"], cfg["H"], cfg["W"], cfg["density"]
+    m = _mask(rng, K, C, 3, 3, d)
+    w = _weights(rng, m)
+    src = _input(rng, N, C, cfg["Hin"], cfg["Win"])
+    b = _bias(rng, K)
+    x = _input(rng, N, C, H, W)
+    return src, Layer("resize_conv_relu_maxpool", x, w, m, b, stride=1, pad=1, relu=True, pool=True)
+
+
 def random_layer(seed: int, N: int, C: int, K: int, H: int, W: int, R: int = 3, S: int = 3, stride: int = 1,
                  pad: int = 1, density: float = 0.2, relu: bool = True, pool: bool = False, bias: bool = True,
                  skew: bool = False) -> Layer:

@@ -34,7 +34,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     assert declared_functions() == sorted(
-        ["spconv_pack_csr", "spconv_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
+        ["spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "spconv_forward", "spconv_forward_ex",
+         "spconv_plan",
          "spconv_output_shape", "spconv_strerror"])
 
 
@@ -205,6 +206,19 @@ def test_forward_and_pad_validate_before_any_gpu_work(sp):
     assert lib.spconv_pad_input(fake, 1, 1, 0, 4, 1, fake, None) == E
     assert lib.spconv_pad_input(fake, 1, 1, 4, 4, -1, fake, None) == E
     assert lib.spconv_pad_input(fake, 1, 1, 4, 4, 1, None, None) == E
+    assert lib.spconv_pad_input(fake, 1, 1, 1, (1 << 31) - 4000, 0, fake, None) == E  # plane above 2^31 - 4096
+    rz = lib.spconv_resize_pad_input
+    assert rz(None, 1, 1, 4, 4, 2, 2, 1, fake, None) == E
+    assert rz(fake, 1, 1, 4, 4, 2, 2, 1, None, None) == E
+    assert rz(fake, 0, 1, 4, 4, 2, 2, 1, fake, None) == E
+    assert rz(fake, 1, 1, 0, 4, 2, 2, 1, fake, None) == E
+    assert rz(fake, 1, 1, 4, 4, 2, 0, 1, fake, None) == E
+    assert rz(fake, 1, 1, 4, 4, 2, 2, -1, fake, None) == E
+    assert rz(fake, 1, 1, 16385, 4, 2, 2, 1, fake, None) == E      # a side above 16384
+    assert rz(fake, 1, 1, 4, 4, 2, 16385, 0, fake, None) == E
+    assert rz(fake, 1, 1, 4, 4, 2, 2, 1 << 15, fake, None) == E    # padded plane of 2^31 elements or more
+    assert rz(fake, 1 << 20, 1 << 10, 4, 4, 32, 32, 0, fake, None) == E  # 2^40 output elements
+    assert rz(fake, 1 << 20, 1 << 10, 32, 32, 2, 2, 0, fake, None) == E  # 2^40 input elements
 
 
 def test_plan_reports_the_launch_without_a_gpu(sp):
