@@ -57,12 +57,25 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shi
 // Padded input (spconv_pad_input)
 // ---------------------------------------------------------------------------
 
-// Streaming stores (nontemporal): the padded tensors are written once, by
-// whole cache lines, and read back by the next kernel; on gfx950 such stores
-// sustain a markedly higher write rate than ordinary ones.
+// Streaming stores (nontemporal): every output tensor of this library is
+// written once, by whole cache lines, and read back (if at all) by the next
+// kernel; on gfx950 such stores sustain a markedly higher write rate than
+// ordinary ones.
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void stream_store(float *p, float v) { __builtin_nontemporal_store(v, p); }
+
+// Output element store of the conv kernels: streaming when the planes are
+// stored without a border (whole lines written by the same kernel's streaming
+// stores); ordinary when a border is written around them, where rows start
+// mid-line and share lines with the border's scattered ordinary stores (mixing
+// the two on one line measured ~10% slower).
+__device__ __forceinline__ void store_out(float *p, float v, bool stream) {
+    if (stream)
+        stream_store(p, v);
+    else
+        *p = v;
+}
 
 __device__ __forceinline__ void stream_store4(float *p, float4 v) {
     const f32x4_t t = {v.x, v.y, v.z, v.w};
@@ -782,7 +795,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
                         float v = (h ? sum[p].y : sum[p].x) + bk;
                         if (rp) v += rp[qq + yl * rdelta];
                         if (a.relu) v = v > 0.0f ? v : 0.0f;
-                        op[qq + yl * odelta] = v;
+                        store_out(op + qq + yl * odelta, v, a.out_pad == 0);
                     }
                 if (a.out_pad)
                     zero_border(plane, y0, min(y0 + a.TH, a.Ho), a.Ho, a.Wo, a.out_pad, a.opitch, ty == 0,
@@ -845,8 +858,9 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
                     if (n < a.N && pr < a.Hq) {
                         const float *s0 = st + im * kImgPx + (2 * r) * a.Wp + 2 * jq;
                         const float m = fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[a.Wp], s0[a.Wp + 1]));
-                        out[((size_t)n * a.K + k) * a.oplane + (size_t)(pr + a.out_pad) * a.opitch + jq + a.out_pad] =
-                            m;
+                        store_out(out + ((size_t)n * a.K + k) * a.oplane + (size_t)(pr + a.out_pad) * a.opitch + jq +
+                                      a.out_pad,
+                                  m, a.out_pad == 0);
                     }
                 }
                 if (a.out_pad)
@@ -978,7 +992,7 @@ __global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, con
                 float v = acc[kk][j] + bk;
                 if (rp) v += rp[q + ylo[j] * rdelta];
                 if (a.relu) v = v > 0.0f ? v : 0.0f;
-                op[q + ylo[j] * odelta] = v;
+                store_out(op + q + ylo[j] * odelta, v, a.out_pad == 0);
             }
             if (a.out_pad && wseg == 0)
                 zero_border(plane, y0, min(y0 + a.TH, a.Ho), a.Ho, a.Wo, a.out_pad, a.opitch, ty == 0,
@@ -1019,7 +1033,9 @@ __global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, con
                 if (nn < a.N && pi < a.Hq) {
                     const float *s0 = lds + im * img_px + (2 * i) * a.wv + 2 * jq;
                     const float m = fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[a.wv], s0[a.wv + 1]));
-                    out[((size_t)nn * a.K + k) * a.oplane + (size_t)(pi + a.out_pad) * a.opitch + jq + a.out_pad] = m;
+                    store_out(out + ((size_t)nn * a.K + k) * a.oplane + (size_t)(pi + a.out_pad) * a.opitch + jq +
+                                  a.out_pad,
+                              m, a.out_pad == 0);
                 }
             }
             if (a.out_pad)
