@@ -23,6 +23,7 @@ sys.path.insert(0, str(ROOT))
 
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E, published
 VALU_FP32_FMA_TFLOPS = 78.6     # 256 CU x 64 lanes x 2 FLOP x 2.4 GHz (v_fma_f32; packed FP32 forms not used)
+MFMA_FP32_TFLOPS = 157.3        # MI355X dense fp32 matrix peak, published
 FP32_VECTOR_PUBLISHED_TFLOPS = 157.3
 
 WORKLOADS = {
@@ -73,22 +74,30 @@ def algorithmic(layer, nnz):
     return flops, fwd_bytes, pad_bytes
 
 
-KERNEL_SOURCE = ROOT / "paper_2005_04091_amd" / "csrc" / "spconv.hip"
+# Sources of each kernel family: their hash keys the committed counter summaries
+# (profiles/spconv_<family>_<workload>_traffic.json).
+KERNEL_SOURCES = {
+    "fwd": [ROOT / "paper_2005_04091_amd" / "csrc" / f for f in ("spconv.hip", "common.h")],
+    "dense": [ROOT / "paper_2005_04091_amd" / "csrc" / f for f in ("dense.hip", "common.h")],
+}
 
 
-def kernel_source_sha() -> str:
-    return hashlib.sha256(KERNEL_SOURCE.read_bytes()).hexdigest()[:16]
+def kernel_source_sha(family: str = "fwd") -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[family]:
+        h.update(f.read_bytes())
+    return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
+def measured_traffic(workload: str, family: str = "fwd"):
     """HBM bytes per launch of the forward kernel, from the committed counter
     summary for this workload, or None when it is missing or was taken on a
     different kernel source."""
-    f = ROOT / "profiles" / f"spconv_fwd_{workload}_traffic.json"
+    f = ROOT / "profiles" / f"spconv_{family}_{workload}_traffic.json"
     if not f.exists():
         return None
     rec = json.loads(f.read_text())
-    if rec.get("kernel_source_sha") != kernel_source_sha():
+    if rec.get("kernel_source_sha") != kernel_source_sha(family):
         return None
     return rec.get("traffic_bytes")
 
@@ -312,6 +321,8 @@ def main():
     ap.add_argument("--workload", default="resnet", choices=sorted(WORKLOADS) + sorted(BLOCKS))
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--path", default="auto", choices=["auto", "sparse", "dense"],
+                    help="kernel family; auto = the library's break-even-density dispatcher")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after timing, copy MIB MiB device-to-device three times (counter calibration)")
     args = ap.parse_args()
@@ -336,8 +347,10 @@ def main():
     N, C, H, W, K, R, S = layer.shape
     print(f"[bench] workload {args.workload}: {WORKLOADS[args.workload]}", file=sys.stderr, flush=True)
     L = spconv.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, layer.stride, layer.pad, layer.relu,
-                               layer.pool, device=dev)
+                               layer.pool, device=dev, path=args.path, N=N)
     nnz = L.host_csr.nnz
+    dense = L.path == "dense"
+    print(f"[bench] path {L.path}: {L.plan(N)}", file=sys.stderr, flush=True)
     x = torch.from_numpy(layer.x).to(dev)
     xp = torch.empty((N, C, H + 2 * layer.pad, W + 2 * layer.pad), dtype=torch.float32, device=dev)
     out = torch.empty((N, K, L.Ho, L.Wo), dtype=torch.float32, device=dev)
@@ -381,7 +394,17 @@ def main():
 
     flops, fwd_bytes, pad_bytes = algorithmic(layer, nnz)
     value = flops / (ms_per_step * 1e-3) / 1e9
-    achieved_tflops = flops / (fwd_avg * 1e-3) / 1e12
+    if dense:
+        # The dense kernel's algorithmic work is every filter tap (its FLOPs on
+        # the stored pixels), on the fp32 matrix cores; its filter read is the
+        # packed dense array instead of the CSR.
+        kern_flops = 2.0 * K * C * R * S * N * (H + 2 * layer.pad - R + 1) * (W + 2 * layer.pad - S + 1)
+        fwd_bytes += 4.0 * L.dense.numel() - (8.0 * nnz)
+        bound, peak, kname = "mfma", MFMA_FP32_TFLOPS, "spconv_dense_kernel"
+    else:
+        kern_flops = flops
+        bound, peak, kname = "alu", VALU_FP32_FMA_TFLOPS, "spconv_fwd_kernel"
+    achieved_tflops = kern_flops / (fwd_avg * 1e-3) / 1e12
     rec = {
         "metric": "ms/layer + nonzero GFLOP/s + % HBM roofline, fused sparse conv, 1 MI355X",
         "value": round(value, 2),
@@ -397,22 +420,22 @@ def main():
         "data": "synthetic (seeded Bernoulli-masked weights U[-1,1), input U[0,1), bias U[-0.1,0.1))",
         "config": {"workload": WORKLOADS[args.workload], "N": N, "C": C, "K": K, "H": H, "W": W, "R": R, "S": S,
                    "stride": layer.stride, "pad": layer.pad, "pool": layer.pool, "nnz": nnz,
-                   "density": round(nnz / (K * C * R * S), 5)},
+                   "density": round(nnz / (K * C * R * S), 5), "path": L.path},
         "ms_per_layer": round(fwd_avg, 5),
         "ms_per_layer_in_step_median": round(fwd_med, 5),
         "ms_pad": round(sum(pad_ms) / len(pad_ms), 5),
         "nonzero_gflops_layer": round(flops / (fwd_avg * 1e-3) / 1e9, 2),
         "hbm_roofline_frac": round(fwd_bytes / (fwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "roofline": {
-            "kernel": "spconv_fwd_kernel",
-            "bound": "alu",
+            "kernel": kname,
+            "bound": bound,
             "achieved": round(achieved_tflops, 3),
-            "peak": VALU_FP32_FMA_TFLOPS,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": round(achieved_tflops / VALU_FP32_FMA_TFLOPS, 4),
-            "traffic": measured_traffic(args.workload),
+            "frac": round(achieved_tflops / peak, 4),
+            "traffic": measured_traffic(args.workload, "dense" if dense else "fwd"),
             "algorithmic_bytes": int(fwd_bytes),
-            "flops": flops,
+            "flops": kern_flops,
         },
     }
     if args.copy_calibration:

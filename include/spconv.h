@@ -211,10 +211,11 @@ int spconv_forward_ex(const float *in_padded, int N, int C, int H, int W, const 
 /* Kernel families reported by spconv_plan. */
 #define SPCONV_KERNEL_STRIDE1 1 /* stride 1: channel-chunked LDS staging, lanes own padded-width pixels */
 #define SPCONV_KERNEL_GENERIC 2 /* any stride */
+#define SPCONV_KERNEL_DENSE 3   /* dense filter on the matrix cores (spconv_forward_dense) */
 
 typedef struct spconv_plan_info {
-    int32_t kernel;                /* SPCONV_KERNEL_STRIDE1 or SPCONV_KERNEL_GENERIC */
-    int32_t pixels_per_lane;       /* virtual output pixels per lane per image */
+    int32_t kernel;                /* SPCONV_KERNEL_STRIDE1, _GENERIC or _DENSE */
+    int32_t pixels_per_lane;       /* virtual output pixels per lane per image; dense: 32-pixel blocks per wave */
     int32_t images_per_group;      /* images sharing one workgroup's tile */
     int32_t channels_per_wave;     /* output channels (CSR rows) per wave; generic kernel: per workgroup */
     int32_t tile_rows;             /* output rows per spatial tile */
@@ -237,6 +238,76 @@ typedef struct spconv_plan_info {
  */
 int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride, int pad,
                 uint32_t flags, spconv_plan_info *info);
+
+/*
+ * Dense path. Above some density, skipping zeros no longer pays: the same
+ * fused convolution computed with every filter tap on the matrix cores
+ * (fp32 MFMA, so the arithmetic stays fp32 like the sparse path) is faster.
+ * The paper reports that its sparse kernels beat the dense ones only below a
+ * break-even density (Evaluation, sparse versus dense, on its CPUs); these
+ * calls give the same choice on MI355X: spconv_select_path predicts which
+ * path is faster for a layer, spconv_forward_dense runs the dense one.
+ */
+#define SPCONV_PATH_SPARSE 1
+#define SPCONV_PATH_DENSE 2
+
+/*
+ * spconv_dense_size - floats of the packed dense filter (host):
+ *   ceil(C/2) * R * S * Kp * 2,  Kp = K rounded up to a multiple of 32 when
+ *   K <= 128, of 128 otherwise.
+ * Errors: SPCONV_EINVAL for a NULL floats, sizes < 1, or 2^40 floats or more.
+ */
+int spconv_dense_size(int K, int C, int R, int S, int64_t *floats);
+
+/*
+ * spconv_pack_dense - the filter in the order spconv_forward_dense reads it
+ * (host): for channel pair cp = c/2, tap t = r*S + s and output channel k,
+ *   packed[((cp*R*S + t)*Kp + k)*2 + c%2] = w[k][c][r][s]
+ * for the entries spconv_pack_csr keeps (same mask rule), 0.0 everywhere else
+ * (absent entries, k >= K, the pad channel of an odd C).
+ * w       [K][C][R][S] fp32, host.   mask  same shape, or NULL (see pack_csr).
+ * packed  host array of packed_len floats, written in full.
+ * Errors: SPCONV_EINVAL (NULL w/packed, bad sizes); SPCONV_ECAPACITY when
+ * packed_len < spconv_dense_size (nothing written).
+ */
+int spconv_pack_dense(const float *w, const uint8_t *mask, int K, int C, int R, int S, float *packed,
+                      int64_t packed_len);
+
+/*
+ * spconv_forward_dense - spconv_forward_ex computed from the packed dense
+ * filter (device, asynchronous): same padded input, bias, flags, epilogue
+ * options, output layout and ordering; the result is the same convolution up
+ * to fp32 summation order. Stride 1 only (the stride is not an argument);
+ * filters 3x3 and 1x1.
+ * packed  device copy of spconv_pack_dense's output for this K, C, R, S.
+ * Errors: SPCONV_EINVAL (NULL in_padded/packed/out, sizes < 1, pad < 0, a
+ * filter other than 3x3 or 1x1, unknown flags, pool with Ho or Wo < 2,
+ * C*Hp*Wp >= 2^31, bad epilogue options as in spconv_forward_ex, or no tiling
+ * that fits the kernel: the padded row wider than 255 floats, 127 with pool);
+ * SPCONV_EHIP when the launch fails.
+ */
+int spconv_forward_dense(const float *in_padded, int N, int C, int H, int W, const float *packed, int K, int R, int S,
+                         int pad, const float *bias, uint32_t flags, const spconv_epilogue *epi, float *out,
+                         hipStream_t stream);
+
+/*
+ * spconv_dense_plan - the launch plan spconv_forward_dense would use (host
+ * only, same checks). Errors: those of spconv_forward_dense; NULL info.
+ */
+int spconv_dense_plan(int N, int C, int H, int W, int K, int R, int S, int pad, uint32_t flags,
+                      spconv_plan_info *info);
+
+/*
+ * spconv_select_path - which path is predicted faster for this layer on
+ * MI355X (host only): SPCONV_PATH_DENSE when the dense kernel applies (stride
+ * 1, 3x3 or 1x1, a plan exists) and the filter density nnz / (K*C*R*S) is
+ * above the break-even density measured on MI355X (0.40; the paper's CPU
+ * figure is 43.5%); otherwise SPCONV_PATH_SPARSE.
+ * Errors: SPCONV_EINVAL for a NULL path, sizes < 1, stride < 1, pad < 0, nnz
+ * outside [0, K*C*R*S], unknown flags.
+ */
+int spconv_select_path(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int64_t nnz,
+                       uint32_t flags, int *path);
 
 /*
  * spconv_output_shape - stored output plane size for the given layer.

@@ -15,7 +15,7 @@ ROOT = PKG.parent
 CSRC = PKG / "csrc"
 INCLUDE = ROOT / "include"
 LIB_PATH = PKG / "libspconv.so"
-SOURCES = [CSRC / "spconv.hip", CSRC / "pack.cpp"]
+SOURCES = [CSRC / "spconv.hip", CSRC / "dense.hip", CSRC / "pack.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

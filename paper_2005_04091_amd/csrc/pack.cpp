@@ -69,3 +69,23 @@ extern "C" int spconv_pack_csr(const float *w, const uint8_t *mask, int K, int C
     }
     return SPCONV_OK;
 }
+
+extern "C" int spconv_pack_dense(const float *w, const uint8_t *mask, int K, int C, int R, int S, float *packed,
+                                 int64_t packed_len) {
+    if (!w || !packed) return SPCONV_EINVAL;
+    int64_t need = 0;
+    const int rc = spconv_dense_size(K, C, R, S, &need);
+    if (rc != SPCONV_OK) return rc;
+    if (packed_len < need) return SPCONV_ECAPACITY;
+    const int64_t RS = (int64_t)R * S;
+    const int64_t Kp = need / ((int64_t)((C + 1) / 2) * RS * 2);
+    std::memset(packed, 0, (size_t)need * sizeof(float));
+    for (int k = 0; k < K; ++k)
+        for (int c = 0; c < C; ++c)
+            for (int64_t t = 0; t < RS; ++t) {
+                const size_t i = ((size_t)k * C + c) * (size_t)RS + (size_t)t;
+                if (!is_entry(w, mask, i)) continue;
+                packed[(((int64_t)(c / 2) * RS + t) * Kp + k) * 2 + (c & 1)] = w[i];
+            }
+    return SPCONV_OK;
+}

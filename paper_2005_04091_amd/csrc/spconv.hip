@@ -36,18 +36,14 @@
 #include <cstdint>
 #include <cstring>
 
+#include "common.h"
 #include "spconv.h"
 
 namespace {
 
-constexpr int kWave = 64;
 constexpr int kWaves = 4;
 constexpr int kThreads = kWave * kWaves;
-constexpr int kXcds = 8;                  // MI355X: 8 XCDs, workgroups dispatched round-robin
 constexpr int kLdsBudgetFloats = 20480;   // generic kernel: 80 KiB of LDS per workgroup (two per CU)
-
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void global_void_t;
 
 __device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shift) {
     return (uint32_t)(((uint64_t)x * (uint64_t)magic) >> shift);
@@ -56,31 +52,6 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shi
 // ---------------------------------------------------------------------------
 // Padded input (spconv_pad_input)
 // ---------------------------------------------------------------------------
-
-// Streaming stores (nontemporal): every output tensor of this library is
-// written once, by whole cache lines, and read back (if at all) by the next
-// kernel; on gfx950 such stores sustain a markedly higher write rate than
-// ordinary ones.
-typedef float f32x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ void stream_store(float *p, float v) { __builtin_nontemporal_store(v, p); }
-
-// Output element store of the conv kernels: streaming when the planes are
-// stored without a border (whole lines written by the same kernel's streaming
-// stores); ordinary when a border is written around them, where rows start
-// mid-line and share lines with the border's scattered ordinary stores (mixing
-// the two on one line measured ~10% slower).
-__device__ __forceinline__ void store_out(float *p, float v, bool stream) {
-    if (stream)
-        stream_store(p, v);
-    else
-        *p = v;
-}
-
-__device__ __forceinline__ void stream_store4(float *p, float4 v) {
-    const f32x4_t t = {v.x, v.y, v.z, v.w};
-    __builtin_nontemporal_store(t, reinterpret_cast<f32x4_t *>(p));
-}
 
 // The padded tensor is treated as one flat array of 4-element quads. A
 // workgroup covers kPadQuads consecutive quads per thread: in round j thread t
@@ -364,39 +335,6 @@ struct FwdArgs {
     int res_pad, rpitch;
     size_t rplane;
 };
-
-// Zero the border of one stored output plane (Hs x Ws inside a border of pd,
-// row pitch `pitch`) for a tile of stored rows [r0, r1): the left and right
-// border columns of those rows, and the top border rows when the tile is the
-// first of the plane, the bottom ones when it is the last. The tiles of a
-// plane partition its rows, so every border element is written exactly once.
-__device__ __forceinline__ void zero_border(float *plane, int r0, int r1, int Hs, int Ws, int pd, int pitch,
-                                            bool first, bool last, int lane, int nlanes) {
-    const int side = (r1 - r0) * 2 * pd;
-    const int top = first ? pd * pitch : 0;
-    const int bottom = last ? pd * pitch : 0;
-    for (int t = lane; t < side + top + bottom; t += nlanes) {
-        int idx;
-        if (t < side) {
-            const int rr = t / (2 * pd), c = t - rr * 2 * pd;
-            idx = (r0 + rr + pd) * pitch + (c < pd ? c : Ws + c);
-        } else if (t < side + top) {
-            idx = t - side;
-        } else {
-            idx = (pd + Hs) * pitch + (t - side - top);
-        }
-        plane[idx] = 0.0f;
-    }
-}
-
-// Workgroup id -> linear work index such that consecutive work items (the
-// channel tiles of one image tile, which read the same input rows) land on the
-// same XCD and therefore share its L2.
-__device__ __forceinline__ int xcd_linear_id(int b, int G) {
-    const int xcd = b % kXcds, i = b / kXcds;
-    const int per = G / kXcds, rem = G % kXcds;
-    return (xcd < rem) ? xcd * (per + 1) + i : rem * (per + 1) + (xcd - rem) * per + i;
-}
 
 // Queue asynchronous global->LDS copies of one channel chunk: for each image of
 // the group and each channel of the chunk, seg_len consecutive floats (the

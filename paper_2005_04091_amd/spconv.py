@@ -25,9 +25,13 @@ SPCONV_RELU = 1
 SPCONV_MAXPOOL2X2 = 2
 
 EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
-            "spconv_output_shape", "spconv_strerror")
+            "spconv_output_shape", "spconv_strerror", "spconv_dense_size", "spconv_pack_dense",
+            "spconv_forward_dense", "spconv_dense_plan", "spconv_select_path")
 SPCONV_KERNEL_STRIDE1 = 1
 SPCONV_KERNEL_GENERIC = 2
+SPCONV_KERNEL_DENSE = 3
+SPCONV_PATH_SPARSE = 1
+SPCONV_PATH_DENSE = 2
 
 
 class spconv_csr(ctypes.Structure):
@@ -80,6 +84,17 @@ def _bind(lib):
                                         ctypes.POINTER(_c_int), ctypes.POINTER(_c_int)]
     lib.spconv_strerror.restype = ctypes.c_char_p
     lib.spconv_strerror.argtypes = [_c_int]
+    lib.spconv_dense_size.restype = _c_int
+    lib.spconv_dense_size.argtypes = [_c_int] * 4 + [ctypes.POINTER(ctypes.c_int64)]
+    lib.spconv_pack_dense.restype = _c_int
+    lib.spconv_pack_dense.argtypes = [_vp, _vp] + [_c_int] * 4 + [_vp, ctypes.c_int64]
+    lib.spconv_forward_dense.restype = _c_int
+    lib.spconv_forward_dense.argtypes = [_vp] + [_c_int] * 4 + [_vp] + [_c_int] * 4 + [
+        _vp, ctypes.c_uint32, ctypes.POINTER(spconv_epilogue), _vp, _vp]
+    lib.spconv_dense_plan.restype = _c_int
+    lib.spconv_dense_plan.argtypes = [_c_int] * 8 + [ctypes.c_uint32, ctypes.POINTER(spconv_plan_info)]
+    lib.spconv_select_path.restype = _c_int
+    lib.spconv_select_path.argtypes = [_c_int] * 9 + [ctypes.c_int64, ctypes.c_uint32, ctypes.POINTER(_c_int)]
     return lib
 
 
@@ -153,6 +168,44 @@ def spconv_pack_csr(w: np.ndarray, mask: np.ndarray | None, Hp: int, Wp: int) ->
     _check(_lib.spconv_pack_csr(_np_ptr(w), _np_ptr(m), K, C, R, S, Hp, Wp, _np_ptr(rowptr), _np_ptr(colidx),
                                 _np_ptr(offset), _np_ptr(vals), n, ctypes.byref(nnz)), "spconv_pack_csr")
     return HostCSR(K, C, R, S, Hp, Wp, rowptr, colidx[:n], offset[:n], vals[:n])
+
+
+def spconv_dense_size(K: int, C: int, R: int, S: int) -> int:
+    n = ctypes.c_int64()
+    _check(_lib.spconv_dense_size(K, C, R, S, ctypes.byref(n)), "spconv_dense_size")
+    return n.value
+
+
+def spconv_pack_dense(w: np.ndarray, mask: np.ndarray | None) -> np.ndarray:
+    """The filter packed for ``spconv_forward_dense`` (host float32 array)."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    if w.ndim != 4:
+        raise ValueError("w must be [K, C, R, S]")
+    K, C, R, S = (int(v) for v in w.shape)
+    m = None
+    if mask is not None:
+        m = np.ascontiguousarray(mask, dtype=np.uint8)
+        if m.shape != w.shape:
+            raise ValueError("mask must have the weight's shape")
+    packed = np.empty(spconv_dense_size(K, C, R, S), np.float32)
+    _check(_lib.spconv_pack_dense(_np_ptr(w), _np_ptr(m), K, C, R, S, _np_ptr(packed), packed.size),
+           "spconv_pack_dense")
+    return packed
+
+
+def spconv_select_path(N: int, C: int, H: int, W: int, K: int, R: int, S: int, stride: int, pad: int, nnz: int,
+                       flags: int) -> int:
+    """SPCONV_PATH_SPARSE or SPCONV_PATH_DENSE: the path predicted faster."""
+    path = _c_int()
+    _check(_lib.spconv_select_path(N, C, H, W, K, R, S, stride, pad, nnz, flags, ctypes.byref(path)),
+           "spconv_select_path")
+    return path.value
+
+
+def spconv_dense_plan(N: int, C: int, H: int, W: int, K: int, R: int, S: int, pad: int, flags: int) -> dict:
+    info = spconv_plan_info()
+    _check(_lib.spconv_dense_plan(N, C, H, W, K, R, S, pad, flags, ctypes.byref(info)), "spconv_dense_plan")
+    return {name: getattr(info, name) for name, _ in spconv_plan_info._fields_}
 
 
 class DeviceCSR:
@@ -270,6 +323,28 @@ def spconv_forward_ex(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int
     return out
 
 
+def spconv_forward_dense(xp, N: int, C: int, H: int, W: int, packed, K: int, R: int, S: int, pad: int, bias=None,
+                         flags: int = SPCONV_RELU, out_pad: int = 0, residual=None, residual_pad: int = 0, out=None,
+                         stream=None):
+    """The fused conv of ``spconv_forward_ex`` from the packed dense filter
+    ``packed`` (device), stride 1."""
+    import torch
+    Hs, Ws = spconv_output_shape(H, W, R, S, 1, pad, flags)
+    if out is None:
+        out = torch.empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), dtype=torch.float32, device=xp.device)
+    Hc, Wc = spconv_output_shape(H, W, R, S, 1, pad, flags & ~SPCONV_MAXPOOL2X2)
+    _check_numel(xp, N * C * (H + 2 * pad) * (W + 2 * pad), "xp")
+    _check_numel(packed, spconv_dense_size(K, C, R, S), "packed")
+    _check_numel(out, N * K * (Hs + 2 * out_pad) * (Ws + 2 * out_pad), "out")
+    _check_numel(bias, K, "bias")
+    _check_numel(residual, N * K * (Hc + 2 * residual_pad) * (Wc + 2 * residual_pad), "residual")
+    epi = spconv_epilogue(out_pad, residual_pad, _dev_ptr(residual, "residual"))
+    _check(_lib.spconv_forward_dense(_dev_ptr(xp, "xp"), N, C, H, W, _dev_ptr(packed, "packed"), K, R, S, pad,
+                                     _dev_ptr(bias, "bias"), flags, ctypes.byref(epi), _dev_ptr(out, "out"),
+                                     _stream_handle(stream, xp.device)), "spconv_forward_dense")
+    return out
+
+
 def spconv_plan(N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int, pad: int,
                 flags: int = SPCONV_RELU) -> dict:
     """The launch plan ``spconv_forward`` would use, as a dict of the
@@ -288,17 +363,33 @@ class SparseConvLayer:
     """One layer's device state: the packed CSR, bias and shape, ready to run.
 
     ``run(x)`` queues pad + fused forward on the current stream and returns the
-    output tensor.
+    output tensor. ``path`` picks the kernel family: "sparse" (the CSR kernels),
+    "dense" (the MFMA kernel on the packed dense filter) or "auto" (the one
+    ``spconv_select_path`` predicts faster for this layer; needs the batch
+    size ``N``). ``self.path`` is the resolved choice.
     """
 
     def __init__(self, w: np.ndarray, mask: np.ndarray | None, bias: np.ndarray | None, H: int, W: int,
-                 stride: int = 1, pad: int = 1, relu: bool = True, pool: bool = False, device="cuda"):
+                 stride: int = 1, pad: int = 1, relu: bool = True, pool: bool = False, device="cuda",
+                 path: str = "sparse", N: int | None = None):
         import torch
         self.K, self.C, self.R, self.S = (int(v) for v in w.shape)
         self.H, self.W, self.stride, self.pad = H, W, stride, pad
         self.flags = flags_of(relu, pool)
         self.host_csr = spconv_pack_csr(w, mask, H + 2 * pad, W + 2 * pad)
+        if path == "auto":
+            if N is None:
+                raise ValueError('path="auto" needs the batch size N')
+            sel = spconv_select_path(N, self.C, H, W, self.K, self.R, self.S, stride, pad, self.host_csr.nnz,
+                                     self.flags)
+            path = "dense" if sel == SPCONV_PATH_DENSE else "sparse"
+        if path not in ("sparse", "dense"):
+            raise ValueError(f"unknown path {path!r}")
+        if path == "dense" and stride != 1:
+            raise ValueError("the dense path is stride 1 only")
+        self.path = path
         self.csr = DeviceCSR(self.host_csr, device)
+        self.dense = torch.from_numpy(spconv_pack_dense(w, mask)).to(device) if path == "dense" else None
         self.bias = None if bias is None else torch.from_numpy(np.ascontiguousarray(bias, np.float32)).to(device)
         self.Ho, self.Wo = spconv_output_shape(H, W, self.R, self.S, stride, pad, self.flags)
 
@@ -315,6 +406,10 @@ class SparseConvLayer:
         ``residual`` (border ``residual_pad``) the shortcut is added before the
         activation."""
         N = int(xp.shape[0])
+        if self.path == "dense":
+            return spconv_forward_dense(xp, N, self.C, self.H, self.W, self.dense, self.K, self.R, self.S, self.pad,
+                                        self.bias, self.flags, out_pad=out_pad, residual=residual,
+                                        residual_pad=residual_pad, out=out, stream=stream)
         if out_pad == 0 and residual is None:
             return spconv_forward(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
                                   self.pad, self.bias, self.flags, out=out, stream=stream)
@@ -323,6 +418,8 @@ class SparseConvLayer:
                                  residual_pad=residual_pad, out=out, stream=stream)
 
     def plan(self, N: int) -> dict:
+        if self.path == "dense":
+            return spconv_dense_plan(N, self.C, self.H, self.W, self.K, self.R, self.S, self.pad, self.flags)
         return spconv_plan(N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride, self.pad,
                            self.flags)
 
