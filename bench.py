@@ -1,8 +1,9 @@
 """Benchmark of the fused sparse convolution on one MI355X.
 
-One step = the whole hot path on one batch: zero-pad the NCHW input
-(spconv_pad_input), then the fused sparse conv + bias + ReLU (+ 2x2 max-pool)
-(spconv_forward). Inputs are seeded synthetic layers already resident in HBM.
+One step = the whole hot path on one batch: zero-pad the NCHW input, then the
+fused sparse conv + bias + ReLU (+ 2x2 max-pool). Where the kernel forms the
+zero border while staging its input (SPCONV_UNPADDED_INPUT) that is one
+launch; otherwise spconv_pad_input, then spconv_forward. Inputs are seeded synthetic layers already resident in HBM.
 Prints one JSON line (rank 0) with the throughput in nonzero GFLOP/s, ms/layer,
 the fraction of the HBM roofline, a roofline record for the dominant kernel and
 the CPU oracle's rate on the same workload.
@@ -164,11 +165,13 @@ def cpu_baseline(layer, budget_s: float):
 
 
 def bench_block(args, dev):
-    """A chained block per step, with inputs resident in HBM: the input is
-    padded once, layer 1 writes layer 2's padded input directly (zero border),
-    layer 2 reads the shortcut from the padded block input (ResNet block). The
-    same block with a separate padding pass between the layers (`unfused`) is
-    timed right after, on the same buffers."""
+    """A chained block per step, with inputs resident in HBM: layer 1 forms its
+    input's zero border in the kernel when its rows are wide enough (else one
+    pad pass comes first) and writes layer 2's padded input directly (zero
+    border); the ResNet shortcut is the unpadded block input. Timed right
+    after, on the same buffers: the same chain after a pad pass, both layers
+    padding in the kernel (two launches), and the unfused block (a pad pass
+    before each layer)."""
     import torch
 
     from paper_2005_04091_amd import spconv, synth
@@ -188,10 +191,26 @@ def bench_block(args, dev):
     stream = torch.cuda.current_stream(dev)
     res = dict(residual=xp, residual_pad=1) if resnet else {}
 
-    def fused():
+    def chained_out_pad():
         L1.pad_input(xd, out=xp, stream=stream)
         L1.forward_padded(xp, out=y1p, stream=stream, out_pad=1)
         L2.forward_padded(y1p, out=y2, stream=stream, **res)
+
+    res_unpadded = dict(residual=xd, residual_pad=0) if resnet else {}
+    l1_in_kernel = L1.pads_in_kernel(N)
+
+    def fused():
+        # Layer 1 pads its input in the kernel when its rows are wide enough,
+        # else after one pad pass; it writes layer 2's zero-bordered input.
+        if l1_in_kernel:
+            L1.forward(xd, out=y1p, stream=stream, out_pad=1)
+            L2.forward_padded(y1p, out=y2, stream=stream, **res_unpadded)
+        else:
+            chained_out_pad()
+
+    def all_in_kernel():
+        L1.forward(xd, out=y1, stream=stream, pad_in_kernel=True)
+        L2.forward(y1, out=y2, stream=stream, pad_in_kernel=True, **res_unpadded)
 
     def unfused():
         L1.pad_input(xd, out=xp, stream=stream)
@@ -212,6 +231,8 @@ def bench_block(args, dev):
         return e0.elapsed_time(e1) / args.steps
 
     ms = timed(fused)
+    ms_chained = timed(chained_out_pad)
+    ms_in_kernel = timed(all_in_kernel)
     ms_unfused = timed(unfused)
     nnz1, nnz2 = L1.host_csr.nnz, L2.host_csr.nnz
     flops = 2.0 * (nnz1 + nnz2) * N * H * W
@@ -231,6 +252,9 @@ def bench_block(args, dev):
         "config": {"workload": BLOCKS[args.workload], "N": N, "C": C, "K": K, "H": H, "W": W,
                    "nnz": [nnz1, nnz2], "pool": bool(l2.pool), "residual": resnet},
         "ms_per_step_unfused": round(ms_unfused, 5),
+        "ms_per_step_chained_out_pad": round(ms_chained, 5),
+        "ms_per_step_both_pad_in_kernel": round(ms_in_kernel, 5),
+        "layer1_pads_in_kernel": l1_in_kernel,
         "fusion_saving_frac": round(1.0 - ms / ms_unfused, 4),
     }
     print(json.dumps(rec), flush=True)
@@ -356,43 +380,50 @@ def main():
     out = torch.empty((N, K, L.Ho, L.Wo), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
-    for _ in range(args.warmup):
-        L.run(x, xp=xp, out=out, stream=stream)
-    torch.cuda.synchronize()
+    # A step is the whole path on one batch. When the layer's kernel forms the
+    # zero border while staging its input (stride-1 and dense kernels), that is
+    # one launch on the unpadded input; otherwise the pad pass, then the
+    # forward on the padded copy.
+    fused_pad = L.pads_in_kernel(N)
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    t_all0 = torch.cuda.Event(enable_timing=True)
-    t_all1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_all0.record(stream)
-    for e0, e1, e2 in ev:
-        e0.record(stream)
+    def step():
+        if fused_pad:
+            L.forward(x, out=out, stream=stream)
+        else:
+            L.pad_input(x, out=xp, stream=stream)
+            L.forward_padded(xp, out=out, stream=stream)
+
+    def separate_pad_step():
         L.pad_input(x, out=xp, stream=stream)
-        e1.record(stream)
         L.forward_padded(xp, out=out, stream=stream)
-        e2.record(stream)
-    t_all1.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_all0.elapsed_time(t_all1)
-    pad_ms = [a.elapsed_time(b) for a, b, _ in ev]
-    fwd_ms = [b.elapsed_time(c) for _, b, c in ev]
-    ms_per_step = total_ms / args.steps
-    fwd_med = statistics.median(fwd_ms)
 
-    # Average duration of one forward launch for the roofline: the same kernel
-    # launched back to back on the same stream, one event pair around all
-    # launches, so that per-launch event and dispatch gaps do not count.
-    f0 = torch.cuda.Event(enable_timing=True)
-    f1 = torch.cuda.Event(enable_timing=True)
-    f0.record(stream)
-    for _ in range(args.steps):
-        L.forward_padded(xp, out=out, stream=stream)
-    f1.record(stream)
-    torch.cuda.synchronize()
-    fwd_avg = f0.elapsed_time(f1) / args.steps
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / args.steps
+
+    ms_per_step = timed(step)
+    ms_separate = timed(separate_pad_step)
+    ms_in_kernel = timed(lambda: L.forward(x, out=out, stream=stream, pad_in_kernel=True)) \
+        if L.can_pad_in_kernel(N) else None
+    pad_only = timed(lambda: L.pad_input(x, out=xp, stream=stream))
+    # Average duration of one forward launch for the roofline: the kernel the
+    # step runs, launched back to back on the same stream, one event pair
+    # around all launches, so that per-launch event and dispatch gaps do not
+    # count (with a separate pad pass: the forward on the padded input).
+    fwd_avg = timed((lambda: L.forward(x, out=out, stream=stream)) if fused_pad
+                    else (lambda: L.forward_padded(xp, out=out, stream=stream)))
 
     flops, fwd_bytes, pad_bytes = algorithmic(layer, nnz)
+    if fused_pad:  # the kernel reads the unpadded input
+        fwd_bytes -= 4.0 * N * C * ((H + 2 * layer.pad) * (W + 2 * layer.pad) - H * W)
     value = flops / (ms_per_step * 1e-3) / 1e9
     if dense:
         # The dense kernel's algorithmic work is every filter tap (its FLOPs on
@@ -420,10 +451,12 @@ def main():
         "data": "synthetic (seeded Bernoulli-masked weights U[-1,1), input U[0,1), bias U[-0.1,0.1))",
         "config": {"workload": WORKLOADS[args.workload], "N": N, "C": C, "K": K, "H": H, "W": W, "R": R, "S": S,
                    "stride": layer.stride, "pad": layer.pad, "pool": layer.pool, "nnz": nnz,
-                   "density": round(nnz / (K * C * R * S), 5), "path": L.path},
+                   "density": round(nnz / (K * C * R * S), 5), "path": L.path, "pad": "fused" if fused_pad else "separate"},
         "ms_per_layer": round(fwd_avg, 5),
-        "ms_per_layer_in_step_median": round(fwd_med, 5),
-        "ms_pad": round(sum(pad_ms) / len(pad_ms), 5),
+        "pad": "in the kernel's LDS staging" if fused_pad else "separate pass",
+        "ms_per_step_separate_pad": round(ms_separate, 5),
+        "ms_per_step_pad_in_kernel": None if ms_in_kernel is None else round(ms_in_kernel, 5),
+        "ms_pad_pass": round(pad_only, 5),
         "nonzero_gflops_layer": round(flops / (fwd_avg * 1e-3) / 1e9, 2),
         "hbm_roofline_frac": round(fwd_bytes / (fwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "roofline": {

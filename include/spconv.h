@@ -37,9 +37,15 @@ extern "C" {
 #define SPCONV_ECAPACITY (-2) /* output arrays too small for the nonzeros (pack) */
 #define SPCONV_EHIP (-3)      /* a HIP call or kernel launch failed */
 
-/* Epilogue flags for spconv_forward. Any other bit is SPCONV_EINVAL. */
+/* Flags for spconv_forward. Any other bit is SPCONV_EINVAL. */
 #define SPCONV_RELU 1u       /* out = max(pre, 0) */
 #define SPCONV_MAXPOOL2X2 2u /* 2x2 window, stride 2, applied after the ReLU */
+/* The input is the unpadded [N][C][H][W] tensor: the kernel forms the zero
+ * border itself while staging the input in LDS, so no padded copy is made
+ * (the pad step fused into the convolution). Stride-1 plans and the dense
+ * path only: a layer whose plan (spconv_plan) is SPCONV_KERNEL_GENERIC gets
+ * SPCONV_EINVAL. The results are bit-identical to the padded input's. */
+#define SPCONV_UNPADDED_INPUT 4u
 
 /*
  * CSR filter (paper, "Sparse Convolution with CSR": flatten (K, C, k, k) to
@@ -141,7 +147,8 @@ int spconv_resize_pad_input(const float *in, int N, int C, int Hin, int Win, int
  *   out = (flags & SPCONV_MAXPOOL2X2) ? max over a,b in {0,1} of o[n,k,2i+a,2j+b] : o
  *
  * in_padded  [N][C][Hp][Wp] fp32, device: the zero-bordered input (as written by
- *            spconv_pad_input).
+ *            spconv_pad_input); with SPCONV_UNPADDED_INPUT the [N][C][H][W]
+ *            input itself.
  * csr        host struct whose arrays are in device memory; csr->K/C/R/S must
  *            equal K/C/R/S and csr->Hp/Wp must equal H+2pad / W+2pad. The array
  *            contents must be a valid CSR as produced by spconv_pack_csr for
@@ -154,7 +161,8 @@ int spconv_resize_pad_input(const float *in, int N, int C, int Hin, int Win, int
  * are reproducible run to run for a given device and shape).
  * Errors: SPCONV_EINVAL (NULL pointer, sizes < 1, stride < 1, pad < 0, shape
  * mismatch with csr, nnz outside [0, 2^31), csr->max_row_nnz outside [0, nnz],
- * unknown flag bits, empty output,
+ * unknown flag bits, SPCONV_UNPADDED_INPUT with a plan other than the
+ * stride-1 kernel, empty output,
  * Ho or Wo < 2 with the pool flag, C*Hp*Wp >= 2^31); SPCONV_EHIP when the
  * launch fails.
  */
@@ -275,7 +283,8 @@ int spconv_pack_dense(const float *w, const uint8_t *mask, int K, int C, int R, 
 
 /*
  * spconv_forward_dense - spconv_forward_ex computed from the packed dense
- * filter (device, asynchronous): same padded input, bias, flags, epilogue
+ * filter (device, asynchronous): same padded (or, with SPCONV_UNPADDED_INPUT,
+ * unpadded) input, bias, flags, epilogue
  * options, output layout and ordering; the result is the same convolution up
  * to fp32 summation order. Stride 1 only (the stride is not an argument);
  * filters 3x3 and 1x1.

@@ -59,6 +59,8 @@ struct DenseArgs {
     size_t oplane;
     int res_pad, rpitch;
     size_t rplane;
+    int unpadded;    // input is N x C x H x W: the border is formed in LDS
+    int H, W, pad, rows_in;
 };
 
 // Queue the copy of one channel chunk of the tile: channel cl of the chunk gets
@@ -73,7 +75,37 @@ __device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__r
     const int nblk = a.PLp / kDnsCopy;
     const size_t plane = (size_t)a.Hp * a.Wp;
     const int nwaves = a.nw * a.ks;
-    for (int u = wave; u < cn * nblk; u += nwaves) {
+    if (a.unpadded) {
+        // Row by row from the unpadded input: padded row row0 + i is image row
+        // row0 + i - pad, written at column pad of the channel's LDS row i, 64
+        // floats per instruction (lanes past the row masked off). Border rows
+        // and columns keep the zeros stored before the first copy.
+        const int segs = (a.W + kWave - 1) / kWave;
+        int cl = 0, i = wave;
+        while (i >= a.rows_in) {
+            i -= a.rows_in;
+            ++cl;
+        }
+        while (cl < cn) {
+            const int y = row0 + i - a.pad;
+            if (y >= 0 && y < a.H) {
+                const float *src = xp + (((size_t)n * a.C + c0 + cl) * a.H + y) * a.W;
+                float *dst = buf + cl * a.PLp + i * a.Wp + a.pad;
+                for (int sg = 0; sg < segs; ++sg) {
+                    const int x0 = sg * kWave;
+                    if (lane < a.W - x0)
+                        __builtin_amdgcn_global_load_lds((global_void_t *)(src + x0 + lane), (lds_void_t *)(dst + x0),
+                                                         4, 0, 0);
+                }
+            }
+            i += nwaves;
+            while (i >= a.rows_in) {
+                i -= a.rows_in;
+                ++cl;
+            }
+        }
+    }
+    for (int u = wave; !a.unpadded && u < cn * nblk; u += nwaves) {
         const int cl = u / nblk, b = u - cl * nblk;
         const size_t first = ((size_t)n * a.C + c0 + cl) * plane + (size_t)row0 * a.Wp + (size_t)b * kDnsCopy;
         const size_t avail = (a.total_floats - first) * sizeof(float);
@@ -122,6 +154,11 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
     // B fragment: the staged channel 2cp + half, pixel 32*b + col, shifted by r*Wp + s.
     const int lane_b = half * a.PLp + col;
 
+    if (a.unpadded) {
+        for (int e = (int)threadIdx.x * 4; e < 2 * a.buf_floats; e += (int)blockDim.x * 4)
+            *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        __syncthreads();
+    }
     dense_stage(a, xp, lds, 0, n, y0, wave, lane);
     dense_wait_copies();
     __syncthreads();
@@ -393,7 +430,7 @@ bool out_extent(int in, int k, int pad, int *o) {
 int prepare_dense(int N, int C, int H, int W, int K, int R, int S, int pad, uint32_t flags,
                   const spconv_epilogue *epi, DensePlan *plp, DenseArgs *ap) {
     if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || pad < 0) return SPCONV_EINVAL;
-    if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2)) return SPCONV_EINVAL;
+    if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2 | SPCONV_UNPADDED_INPUT)) return SPCONV_EINVAL;
     const long long Hp = (long long)H + 2LL * pad, Wp = (long long)W + 2LL * pad;
     if ((long long)C * Hp * Wp >= (1LL << 31)) return SPCONV_EINVAL;
     const bool pool = (flags & SPCONV_MAXPOOL2X2) != 0;
@@ -415,6 +452,11 @@ int prepare_dense(int N, int C, int H, int W, int K, int R, int S, int pad, uint
     a.Hq = pool ? Ho / 2 : Ho;
     a.Wq = pool ? Wo / 2 : Wo;
     a.relu = (flags & SPCONV_RELU) ? 1 : 0;
+    a.unpadded = (flags & SPCONV_UNPADDED_INPUT) ? 1 : 0;
+    a.H = H;
+    a.W = W;
+    a.pad = pad;
+    a.rows_in = pl.TH + R - 1;
     a.TH = pl.TH;
     a.ntiles_y = pl.ntiles_y;
     a.nw = pl.nw;
@@ -507,13 +549,14 @@ constexpr double kBreakEvenDensity = 0.40;
 extern "C" int spconv_select_path(int N, int C, int H, int W, int K, int R, int S, int stride, int pad, int64_t nnz,
                                   uint32_t flags, int *path) {
     if (!path || N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 || pad < 0 || nnz < 0 ||
-        nnz > (int64_t)K * C * R * S || (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2)))
+        nnz > (int64_t)K * C * R * S || (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2 | SPCONV_UNPADDED_INPUT)))
         return SPCONV_EINVAL;
     *path = SPCONV_PATH_SPARSE;
     if (stride != 1) return SPCONV_OK;
     DensePlan pl;
     DenseArgs a;
-    if (prepare_dense(N, C, H, W, K, R, S, pad, flags, nullptr, &pl, &a) != SPCONV_OK) return SPCONV_OK;
+    if (prepare_dense(N, C, H, W, K, R, S, pad, flags & ~SPCONV_UNPADDED_INPUT, nullptr, &pl, &a) != SPCONV_OK)
+        return SPCONV_OK;
     if ((double)nnz > kBreakEvenDensity * (double)K * C * R * S) *path = SPCONV_PATH_DENSE;
     return SPCONV_OK;
 }

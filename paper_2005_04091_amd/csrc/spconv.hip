@@ -334,6 +334,17 @@ struct FwdArgs {
     size_t oplane;
     int res_pad, rpitch;
     size_t rplane;
+    // input layout: 0 = padded (N x C x Hp x Wp); 1 = unpadded (N x C x H x W),
+    // the zero border formed in LDS by the stride-1 kernel's staging
+    int unpadded;
+    int H, W, pad;
+    // stride-1 kernel: pitch of the virtual tile and of the staged LDS rows
+    // (Wp, or Wp rounded up to 4 for 16-byte row copies of an unpadded input),
+    // the LDS column of padded column 0 (lds_shift), and whether rows are
+    // copied 16 bytes per lane
+    int vp, lds_shift, dma16;
+    uint32_t wp_magic;  // x / Wp == (x * wp_magic) >> wp_shift
+    int wp_shift;
 };
 
 // Queue asynchronous global->LDS copies of one channel chunk: for each image of
@@ -380,6 +391,57 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
                                                int ig, int in_row0, int wave, int lane) {
     const int c0 = ch * a.Cc;
     const int cn = min(a.Cc, a.C - c0);
+    if (a.unpadded) {
+        // From the unpadded input: padded row in_row0 + i of the tile is image
+        // row y = in_row0 + i - pad; its W floats land at column pad of the
+        // channel's LDS row i, 64 per instruction (one dword per lane, lanes
+        // past the row masked off). Rows outside the image and the border
+        // columns are never written: they keep the zeros the kernel stored
+        // in both buffers before the first copy.
+        // Units are (channel, row) pairs, dealt round-robin to the waves; a
+        // unit copies its row in segments of 64 lanes: 16 bytes per lane when
+        // rows are 16-byte aligned in HBM and LDS (dma16), else 4.
+        const int per_lane = a.dma16 ? 4 : 1;
+        const int seg_floats = kWave * per_lane;
+        const int segs = (a.W + seg_floats - 1) / seg_floats;
+        int cl = 0, i = wave;
+        while (i >= a.rows_in) {
+            i -= a.rows_in;
+            ++cl;
+        }
+        for (; cl < cn; ) {
+            const int y = in_row0 + i - a.pad;
+            if (y >= 0 && y < a.H) {
+                for (int im = 0; im < a.ipw; ++im) {
+                    const int nn = ig * a.ipw + im;
+                    if (nn >= a.N) break;
+                    const float *src = xp + (((size_t)nn * a.C + c0 + cl) * a.H + y) * a.W;
+                    float *dst = buf + im * a.img_lds + cl * a.PLp + a.lds_shift + i * a.vp + a.pad;
+                    for (int sg = 0; sg < segs; ++sg) {
+                        const int x0 = sg * seg_floats;
+                        if (lane * per_lane < a.W - x0) {
+                            if (a.dma16) {
+                                __amdgpu_buffer_rsrc_t rsrc =
+                                    __builtin_amdgcn_make_buffer_rsrc((void *)(src + x0), (short)0, (a.W - x0) * 4,
+                                                                      0x00020000);
+                                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(dst + x0), 16, lane * 16,
+                                                                         0, 0, 0);
+                            } else {
+                                __builtin_amdgcn_global_load_lds((global_void_t *)(src + x0 + lane),
+                                                                 (lds_void_t *)(dst + x0), 4, 0, 0);
+                            }
+                        }
+                    }
+                }
+            }
+            i += kS1Waves;
+            while (i >= a.rows_in) {
+                i -= a.rows_in;
+                ++cl;
+            }
+        }
+        return;
+    }
     const int nblk = a.PLp / kStageBlock;
     const int plane = a.Hp * a.Wp;
     for (int im = 0; im < a.ipw; ++im) {
@@ -454,7 +516,10 @@ __device__ __forceinline__ Window decode_window(const FwdArgs &a, const RawWindo
         const int o = r.o[h];
         const bool in = r.base + h * kWave + lane < e && o < bound;
         const int c = (int)fast_div((uint32_t)o, a.magic, a.shift);
-        const int t = vb + o - c * a.plane_delta;
+        // LDS index of the tap for virtual pixel 0: channel slot c*PLp, then
+        // the tap (r, s) at r*vp + s + lds_shift (o - c*Hp*Wp = r*Wp + s).
+        const int tap_row = (int)fast_div((uint32_t)(o - c * a.Hp * a.Wp), a.wp_magic, a.wp_shift);
+        const int t = vb + o - c * a.plane_delta + tap_row * (a.vp - a.Wp) + a.lds_shift;
         const int odd = t & 1;
         win.lo[h] = t - odd;
         // Touch the loaded weight here, so that the wait for its load is
@@ -640,6 +705,13 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 
     Window win[RPW];
     RawWindow next[RPW];
+    if (a.unpadded) {
+        // Zero both chunk buffers once: the staging of an unpadded input never
+        // writes the border positions, which must read as the zero padding.
+        for (int e = (int)threadIdx.x * 4; e < 2 * a.buf_floats; e += kS1Threads * 4)
+            *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        __syncthreads();
+    }
     stage_chunk_s1(a, xp, lds, 0, ig, y0, wave, lane);
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
@@ -692,10 +764,10 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
         }
     }
 
-    const int tile_px = a.TH * a.Wp;
+    const int tile_px = a.TH * a.vp;
     if constexpr (!POOL) {
         // Tile row of each of this lane's pixels, or -1 when the pixel is not
-        // stored. Pixel qq = yl*Wp + x of the tile lands at qq + yl*(pitch - Wp)
+        // stored. Pixel qq = yl*vp + x of the tile lands at qq + yl*(pitch - vp)
         // past the tile's first element, in the output and the residual alike.
         int ylo[PJ][2];
 #pragma unroll
@@ -703,10 +775,10 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int qq = q + 2 * kWave * p + h;
-                const int yl = qq / a.Wp, x = qq - yl * a.Wp;
+                const int yl = qq / a.vp, x = qq - yl * a.vp;
                 ylo[p][h] = (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) ? yl : -1;
             }
-        const int odelta = a.opitch - a.Wp, rdelta = a.rpitch - a.Wp;
+        const int odelta = a.opitch - a.vp, rdelta = a.rpitch - a.vp;
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             const int k = krow[i];
@@ -773,8 +845,8 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 #pragma unroll
                         for (int h = 0; h < 2; ++h) {
                             const int qq = q + 2 * kWave * p + h;
-                            const int yl = qq / a.Wp, x = qq - yl * a.Wp;
-                            if (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) v[h] += rp[qq + yl * (a.rpitch - a.Wp)];
+                            const int yl = qq / a.vp, x = qq - yl * a.vp;
+                            if (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) v[h] += rp[qq + yl * (a.rpitch - a.vp)];
                         }
                     }
                     if (a.relu) {
@@ -794,8 +866,8 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
                     const int n = ig * IPW + im;
                     const int pr = prow0 + r;
                     if (n < a.N && pr < a.Hq) {
-                        const float *s0 = st + im * kImgPx + (2 * r) * a.Wp + 2 * jq;
-                        const float m = fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[a.Wp], s0[a.Wp + 1]));
+                        const float *s0 = st + im * kImgPx + (2 * r) * a.vp + 2 * jq;
+                        const float m = fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[a.vp], s0[a.vp + 1]));
                         store_out(out + ((size_t)n * a.K + k) * a.oplane + (size_t)(pr + a.out_pad) * a.opitch + jq +
                                       a.out_pad,
                                   m, a.out_pad == 0);
@@ -1082,9 +1154,11 @@ FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool) {
 // The constants were fitted to measured run times of 5-7 tilings each of
 // ResNet, VGG (with and without pooling), conv+pool and narrow 256-channel
 // layers, so that the model orders each layer's tilings as measured.
-bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, int S, bool pool, long long nnz,
-                  long long max_row_nnz, Plan *out) {
-    const int img_pix = Ho * Wp;
+// vp: pitch of the virtual tile and of the staged LDS rows; shift: LDS column
+// of padded column 0 (both Wp and 0 for a padded input).
+bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho, int Wo, int R, int S, bool pool,
+                  long long nnz, long long max_row_nnz, Plan *out) {
+    const int img_pix = Ho * vp;
     const double row_nnz = std::max(1.0, (double)nnz / K);
     const double skew = max_row_nnz > 0 ? (double)max_row_nnz / row_nnz : 1.0;
     Plan best;
@@ -1100,7 +1174,7 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, in
             nt = 1;
         } else {
             if (IPW != 1) return;
-            int th_max = (cap - 1) / Wp;
+            int th_max = (cap - 1) / vp;
             if (pool) th_max &= ~1;
             if (th_max < 1) return;
             nt = ceil_div(Ho, th_max);
@@ -1109,11 +1183,11 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, in
             nt = ceil_div(Ho, TH);
         }
         const int rows_in = TH + R - 1;
-        const int PL = rows_in * Wp;
+        const int PL = rows_in * vp + shift;
         const int PLp = ceil_div(PL, kStageBlock) * kStageBlock;
-        // Lanes past the tile read up to cap - TH*Wp + S - 2 floats beyond the
+        // Lanes past the tile read up to cap - TH*vp + S - 2 floats beyond the
         // last image block; keep that inside the buffer.
-        const int slack = cap - TH * Wp + S;
+        const int slack = cap - TH * vp + S;
         const int per_buf = kS1LdsFloats / 2;
         int cc_max = (per_buf - slack) / (IPW * PLp);
         if (cc_max < 1) return;
@@ -1147,7 +1221,7 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int R, in
             best.PLp = PLp;
             best.img_lds = Cc * PLp;
             best.buf_floats = ceil_div(IPW * Cc * PLp + slack, 64) * 64;
-            best.wv = Wp;
+            best.wv = vp;
             best.rows_per_wg = KT;
             best.nktiles = ceil_div(K, KT);
             best.total_wgs = (int)wgs;
@@ -1247,7 +1321,7 @@ bool out_extent(int in, int f, int stride, int pad, int *o) {
 
 extern "C" int spconv_output_shape(int H, int W, int R, int S, int stride, int pad, uint32_t flags, int *Ho, int *Wo) {
     if (!Ho || !Wo || H < 1 || W < 1 || R < 1 || S < 1 || stride < 1 || pad < 0) return SPCONV_EINVAL;
-    if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2)) return SPCONV_EINVAL;
+    if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2 | SPCONV_UNPADDED_INPUT)) return SPCONV_EINVAL;
     int ho, wo;
     if (!out_extent(H, R, stride, pad, &ho) || !out_extent(W, S, stride, pad, &wo)) return SPCONV_EINVAL;
     if (flags & SPCONV_MAXPOOL2X2) {
@@ -1362,7 +1436,7 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
                     uint32_t flags, Plan *plp, FwdArgs *ap) {
     if (!csr) return SPCONV_EINVAL;
     if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 || pad < 0) return SPCONV_EINVAL;
-    if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2)) return SPCONV_EINVAL;
+    if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2 | SPCONV_UNPADDED_INPUT)) return SPCONV_EINVAL;
     if (csr->K != K || csr->C != C || csr->R != R || csr->S != S) return SPCONV_EINVAL;
     const long long Hp = (long long)H + 2LL * pad, Wp = (long long)W + 2LL * pad;
     if (csr->Hp != Hp || csr->Wp != Wp) return SPCONV_EINVAL;
@@ -1376,12 +1450,37 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     if (Ho < 1 || Wo < 1) return SPCONV_EINVAL;
     if (pool && (Ho < 2 || Wo < 2)) return SPCONV_EINVAL;
 
+    // An unpadded input whose rows are a whole number of 16-byte groups is
+    // staged with 16-byte row copies: the LDS rows then take a pitch vp that
+    // is a multiple of 4 floats, and padded column 0 sits at LDS column shift,
+    // so that every row's first image column is 16-byte aligned.
+    const bool unpadded = (flags & SPCONV_UNPADDED_INPUT) != 0;
+    bool row16 = unpadded && stride == 1 && W % 4 == 0;
     Plan pl;
-    const bool ok = (stride == 1) ? plan_stride1(N, C, K, (int)Hp, (int)Wp, Ho, Wo, R, S, pool, csr->nnz,
-                                                 csr->max_row_nnz, &pl)
-                                  : plan_generic(N, C, K, (int)Hp, (int)Wp, Ho, Wo, stride, R, pool, &pl);
+    bool ok = false;
+    if (stride != 1) {
+        ok = plan_generic(N, C, K, (int)Hp, (int)Wp, Ho, Wo, stride, R, pool, &pl);
+    } else {
+        if (row16)
+            ok = plan_stride1(N, C, K, (int)Hp, (int)Wp, ((int)Wp + 3) / 4 * 4, (4 - pad % 4) % 4, Ho, Wo, R, S,
+                              pool, csr->nnz, csr->max_row_nnz, &pl);
+        if (!ok) {
+            row16 = false;
+            ok = plan_stride1(N, C, K, (int)Hp, (int)Wp, (int)Wp, 0, Ho, Wo, R, S, pool, csr->nnz, csr->max_row_nnz,
+                              &pl);
+        }
+    }
     if (!ok) return SPCONV_EINVAL;
+    if (unpadded && pl.kind != Kind::kStride1) return SPCONV_EINVAL;
     FwdArgs a;
+    a.unpadded = unpadded ? 1 : 0;
+    a.vp = pl.kind == Kind::kStride1 ? pl.wv : (int)Wp;
+    a.lds_shift = row16 ? (4 - pad % 4) % 4 : 0;
+    a.dma16 = row16 ? 1 : 0;
+    if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift)) return SPCONV_EINVAL;
+    a.H = H;
+    a.W = W;
+    a.pad = pad;
     a.N = N;
     a.C = C;
     a.K = K;
@@ -1455,6 +1554,9 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
     rc = apply_epilogue(epi, &a);
     if (rc != SPCONV_OK) return rc;
     const float *residual = epi ? epi->residual : nullptr;
+    // 16-byte row copies need a 16-byte aligned tensor; otherwise the same
+    // layout is filled 4 bytes per lane.
+    if (a.dma16 && (reinterpret_cast<uintptr_t>(in_padded) & 15) != 0) a.dma16 = 0;
     FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0);
     const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
     if (pl.lds_bytes > 65536 &&

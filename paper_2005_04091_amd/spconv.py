@@ -23,6 +23,7 @@ SPCONV_ECAPACITY = -2
 SPCONV_EHIP = -3
 SPCONV_RELU = 1
 SPCONV_MAXPOOL2X2 = 2
+SPCONV_UNPADDED_INPUT = 4
 
 EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
             "spconv_output_shape", "spconv_strerror", "spconv_dense_size", "spconv_pack_dense",
@@ -247,6 +248,12 @@ def _check_numel(t, n, name):
         raise ValueError(f"{name} holds {t.numel()} elements, the call needs {n}")
 
 
+def _in_elems(N, C, H, W, pad, flags):
+    """Elements of the forward input: padded, or the raw tensor with SPCONV_UNPADDED_INPUT."""
+    p = 0 if flags & SPCONV_UNPADDED_INPUT else pad
+    return N * C * (H + 2 * p) * (W + 2 * p)
+
+
 def _stream_handle(stream, device):
     import torch
     s = stream if stream is not None else torch.cuda.current_stream(device)
@@ -291,7 +298,7 @@ def spconv_forward(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R
     Ho, Wo = spconv_output_shape(H, W, R, S, stride, pad, flags)
     if out is None:
         out = torch.empty((N, K, Ho, Wo), dtype=torch.float32, device=xp.device)
-    _check_numel(xp, N * C * (H + 2 * pad) * (W + 2 * pad), "xp")
+    _check_numel(xp, _in_elems(N, C, H, W, pad, flags), "xp")
     _check_numel(out, N * K * Ho * Wo, "out")
     _check_numel(bias, K, "bias")
     _check(_lib.spconv_forward(_dev_ptr(xp, "xp"), N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad,
@@ -312,7 +319,7 @@ def spconv_forward_ex(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int
     if out is None:
         out = torch.empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), dtype=torch.float32, device=xp.device)
     Hc, Wc = spconv_output_shape(H, W, R, S, stride, pad, flags & ~SPCONV_MAXPOOL2X2)
-    _check_numel(xp, N * C * (H + 2 * pad) * (W + 2 * pad), "xp")
+    _check_numel(xp, _in_elems(N, C, H, W, pad, flags), "xp")
     _check_numel(out, N * K * (Hs + 2 * out_pad) * (Ws + 2 * out_pad), "out")
     _check_numel(bias, K, "bias")
     _check_numel(residual, N * K * (Hc + 2 * residual_pad) * (Wc + 2 * residual_pad), "residual")
@@ -333,7 +340,7 @@ def spconv_forward_dense(xp, N: int, C: int, H: int, W: int, packed, K: int, R: 
     if out is None:
         out = torch.empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), dtype=torch.float32, device=xp.device)
     Hc, Wc = spconv_output_shape(H, W, R, S, 1, pad, flags & ~SPCONV_MAXPOOL2X2)
-    _check_numel(xp, N * C * (H + 2 * pad) * (W + 2 * pad), "xp")
+    _check_numel(xp, _in_elems(N, C, H, W, pad, flags), "xp")
     _check_numel(packed, spconv_dense_size(K, C, R, S), "packed")
     _check_numel(out, N * K * (Hs + 2 * out_pad) * (Ws + 2 * out_pad), "out")
     _check_numel(bias, K, "bias")
@@ -400,22 +407,64 @@ class SparseConvLayer:
         """Bilinear resize of ``x`` to this layer's H x W, written as its padded input."""
         return spconv_resize_pad_input(x, self.H, self.W, self.pad, out=out, stream=stream)
 
-    def forward_padded(self, xp, out=None, stream=None, out_pad: int = 0, residual=None, residual_pad: int = 0):
+    def forward_padded(self, xp, out=None, stream=None, out_pad: int = 0, residual=None, residual_pad: int = 0,
+                       _extra_flags: int = 0):
         """Fused forward on the padded input. With ``out_pad`` the output planes
         carry that zero border (ready as the next layer's padded input); with
         ``residual`` (border ``residual_pad``) the shortcut is added before the
         activation."""
         N = int(xp.shape[0])
+        flags = self.flags | _extra_flags
         if self.path == "dense":
             return spconv_forward_dense(xp, N, self.C, self.H, self.W, self.dense, self.K, self.R, self.S, self.pad,
-                                        self.bias, self.flags, out_pad=out_pad, residual=residual,
+                                        self.bias, flags, out_pad=out_pad, residual=residual,
                                         residual_pad=residual_pad, out=out, stream=stream)
         if out_pad == 0 and residual is None:
             return spconv_forward(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
-                                  self.pad, self.bias, self.flags, out=out, stream=stream)
+                                  self.pad, self.bias, flags, out=out, stream=stream)
         return spconv_forward_ex(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
-                                 self.pad, self.bias, self.flags, out_pad=out_pad, residual=residual,
+                                 self.pad, self.bias, flags, out_pad=out_pad, residual=residual,
                                  residual_pad=residual_pad, out=out, stream=stream)
+
+    # The kernels stage an unpadded input one image row per LDS-DMA instruction,
+    # and on MI355X such a copy costs about the same per instruction up to 1
+    # KiB; rows narrower than this many bytes make the copies slower than a
+    # separate pad pass (measured: 224-byte rows 3.4x the time of 1 KiB
+    # copies for the same bytes, 896-byte rows on par).
+    MIN_ROW_BYTES_PAD_IN_KERNEL = 768
+
+    def can_pad_in_kernel(self, N: int) -> bool:
+        """Whether this layer's kernel can form the zero border itself (the
+        dense kernel and stride-1 sparse plans)."""
+        cache = self.__dict__.setdefault("_can_pad_in_kernel", {})
+        if N not in cache:
+            cache[N] = self.path == "dense" or self.plan(N)["kernel"] == SPCONV_KERNEL_STRIDE1
+        return cache[N]
+
+    def pads_in_kernel(self, N: int) -> bool:
+        """Whether ``forward`` forms the zero border in the kernel (it can, and
+        the rows are wide enough for that to beat a pad pass)."""
+        return self.can_pad_in_kernel(N) and 4 * self.W >= self.MIN_ROW_BYTES_PAD_IN_KERNEL
+
+    def forward(self, x, out=None, stream=None, out_pad: int = 0, residual=None, residual_pad: int = 0, xp=None,
+                pad_in_kernel: bool | None = None):
+        """Fused forward on the unpadded NCHW input ``x``: the kernel forms the
+        zero border while staging the input (SPCONV_UNPADDED_INPUT), or a pad
+        pass into ``xp`` comes first. ``pad_in_kernel`` None picks the faster
+        (``pads_in_kernel``); True requires the kernel path."""
+        N = int(x.shape[0])
+        if pad_in_kernel is None:
+            pad_in_kernel = self.pads_in_kernel(N)
+        if pad_in_kernel and not self.can_pad_in_kernel(N):
+            raise ValueError("this layer's kernel cannot pad its input (any-stride plan)")
+        if pad_in_kernel:
+            if x.dim() != 4 or tuple(int(v) for v in x.shape[1:]) != (self.C, self.H, self.W):
+                raise ValueError("x must be [N, C, H, W] of this layer")
+            return self.forward_padded(x, out=out, stream=stream, out_pad=out_pad, residual=residual,
+                                       residual_pad=residual_pad, _extra_flags=SPCONV_UNPADDED_INPUT)
+        xp = self.pad_input(x, out=xp, stream=stream)
+        return self.forward_padded(xp, out=out, stream=stream, out_pad=out_pad, residual=residual,
+                                   residual_pad=residual_pad)
 
     def plan(self, N: int) -> dict:
         if self.path == "dense":

@@ -140,7 +140,8 @@ def test_output_shape(sp):
     assert sp.spconv_output_shape(28, 28, 3, 3, 1, 1, sp.SPCONV_RELU | sp.SPCONV_MAXPOOL2X2) == (14, 14)
     assert sp.spconv_output_shape(7, 9, 3, 3, 2, 1, 0) == (4, 5)
     assert sp.spconv_output_shape(5, 5, 3, 3, 1, 1, sp.SPCONV_MAXPOOL2X2) == (2, 2)  # odd: floor
-    for bad in [(0, 5, 3, 3, 1, 1, 0), (5, 5, 3, 3, 0, 1, 0), (5, 5, 3, 3, 1, -1, 0), (5, 5, 3, 3, 1, 1, 4),
+    assert sp.spconv_output_shape(56, 56, 3, 3, 1, 1, sp.SPCONV_RELU | sp.SPCONV_UNPADDED_INPUT) == (56, 56)
+    for bad in [(0, 5, 3, 3, 1, 1, 0), (5, 5, 3, 3, 0, 1, 0), (5, 5, 3, 3, 1, -1, 0), (5, 5, 3, 3, 1, 1, 8),
                 (2, 2, 3, 3, 1, 0, 0), (3, 3, 3, 3, 1, 0, sp.SPCONV_MAXPOOL2X2)]:
         with pytest.raises(sp.SpconvError) as e:
             sp.spconv_output_shape(*bad)
@@ -176,6 +177,7 @@ def test_forward_and_pad_validate_before_any_gpu_work(sp):
     assert fwd(stride=0) == E
     assert fwd(pad=-1) == E
     assert fwd(flags=8) == E
+    assert fwd(stride=2, flags=1 | sp.SPCONV_UNPADDED_INPUT) == E  # unpadded input: stride-1 plans only
     assert fwd(K=5) == E            # csr->K mismatch
     assert fwd(C=4) == E            # csr->C mismatch
     assert fwd(H=9) == E            # csr->Hp != H + 2 pad
