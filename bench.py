@@ -116,19 +116,59 @@ def copy_calibration(mb: int, dev):
     torch.cuda.synchronize()
 
 
-def cpu_baseline(layer, budget_s: float):
+def cold_median_ms(fn, stream, reps: int, dev) -> float:
+    """Median duration of `fn` with the last-level cache flushed before each
+    run: a 512 MiB buffer is written first (the 256 MB MALL cannot hold the
+    layer's input from the previous run), then a HIP event pair on the launch
+    stream brackets `fn` alone."""
+    import torch
+    flush = torch.empty(512 * 1024 * 1024 // 4, dtype=torch.float32, device=dev)
+    times = []
+    for i in range(reps):
+        flush.fill_(float(i))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del flush
+    return statistics.median(times)
+
+
+def measured_copy_gbs(dev) -> float:
+    """Device-to-device copy rate of a 512 MiB buffer (read + write bytes per
+    second, best of 5): the practical HBM ceiling beside the 8 TB/s spec."""
+    import torch
+    n = 512 * 1024 * 1024 // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    best = None
+    for _ in range(6):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1)
+        best = t if best is None else min(best, t)
+    del src, dst
+    return 2.0 * n * 4 / (best * 1e-3) / 1e9
+
+
+def cpu_baseline(layer, budget_s: float, nthreads: int = 0):
     """Time the CPU oracle (as it stands) on a bounded sample of the same layer.
 
     If the whole layer takes less than the budget, whole-layer passes are
     repeated until the budget is spent and the median pass is reported;
     otherwise a random subset of output planes (n, k) sized to the budget runs
-    once. Threads: the OpenMP default of this process."""
+    once. Threads: `nthreads`, or the OpenMP default of this process (0)."""
     import numpy as np
     import oracle
 
     N, C, H, W, K, R, S = layer.shape
     orc = oracle.get()
-    threads = orc.max_threads()
+    threads = nthreads if nthreads > 0 else orc.max_threads()
     total = N * K
     Hp, Wp = H + 2 * layer.pad, W + 2 * layer.pad
     Ho = (Hp - R) // layer.stride + 1
@@ -138,7 +178,7 @@ def cpu_baseline(layer, budget_s: float):
     def run(pairs):
         t0 = time.perf_counter()
         orc.conv(layer.x, layer.w, layer.mask, layer.bias, layer.stride, layer.pad, layer.relu, layer.pool,
-                 pairs=pairs)
+                 pairs=pairs, nthreads=nthreads)
         return time.perf_counter() - t0
 
     rng = np.random.default_rng(0)
@@ -345,6 +385,8 @@ def main():
     ap.add_argument("--workload", default="resnet", choices=sorted(WORKLOADS) + sorted(BLOCKS))
     ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold", action="store_true",
+                    help="also report the forward's median over 30 runs with the last-level cache flushed before each")
     ap.add_argument("--compare", action="store_true",
                     help="also time the step with a separate pad pass and with the pad formed in the kernel")
     ap.add_argument("--path", default="auto", choices=["auto", "sparse", "dense"],
@@ -425,6 +467,13 @@ def main():
     fwd_avg = timed((lambda: L.forward(x, out=out, stream=stream)) if fused_pad
                     else (lambda: L.forward_padded(xp, out=out, stream=stream)))
 
+    # The same forward with a cold last-level cache (median of 30, as the paper
+    # reports medians), and the measured copy ceiling.
+    fwd_fn = (lambda: L.forward(x, out=out, stream=stream)) if fused_pad \
+        else (lambda: L.forward_padded(xp, out=out, stream=stream))
+    fwd_cold = cold_median_ms(fwd_fn, stream, 30, dev) if args.cold else None
+    copy_gbs = measured_copy_gbs(dev)
+
     flops, fwd_bytes, pad_bytes = algorithmic(layer, nnz)
     if fused_pad:  # the kernel reads the unpadded input
         fwd_bytes -= 4.0 * N * C * ((H + 2 * layer.pad) * (W + 2 * layer.pad) - H * W)
@@ -463,6 +512,9 @@ def main():
         "ms_pad_pass": round(pad_only, 5),
         "nonzero_gflops_layer": round(flops / (fwd_avg * 1e-3) / 1e9, 2),
         "hbm_roofline_frac": round(fwd_bytes / (fwd_avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "ms_per_layer_cold_median": None if fwd_cold is None else round(fwd_cold, 5),
+        "hbm_copy_measured_GBs": round(copy_gbs, 1),
+        "hbm_frac_of_measured_copy": round(fwd_bytes / (fwd_avg * 1e-3) / 1e9 / copy_gbs, 4),
         "roofline": {
             "kernel": kname,
             "bound": bound,
@@ -482,6 +534,9 @@ def main():
         cb = cpu_baseline(layer, args.cpu_budget)
         cb["value"] = round(cb["value"], 3)
         rec["cpu_baseline"] = cb
+        cb1 = cpu_baseline(layer, args.cpu_budget / 2, nthreads=1)
+        cb1["value"] = round(cb1["value"], 3)
+        rec["cpu_baseline_1thread"] = cb1
     print(json.dumps(rec), flush=True)
 
 
