@@ -291,7 +291,8 @@ int spconv_pack_dense(const float *w, const uint8_t *mask, int K, int C, int R, 
  * packed  device copy of spconv_pack_dense's output for this K, C, R, S.
  * Errors: SPCONV_EINVAL (NULL in_padded/packed/out, sizes < 1, pad < 0, a
  * filter other than 3x3 or 1x1, unknown flags, pool with Ho or Wo < 2,
- * C*Hp*Wp >= 2^31, bad epilogue options as in spconv_forward_ex, or no tiling
+ * C*Hp*Wp >= 2^31, a packed filter of 2^31 bytes or more, bad epilogue
+ * options as in spconv_forward_ex, or no tiling
  * that fits the kernel: the padded row wider than 255 floats, 127 with pool);
  * SPCONV_EHIP when the launch fails.
  */
@@ -310,8 +311,10 @@ int spconv_dense_plan(int N, int C, int H, int W, int K, int R, int S, int pad, 
  * spconv_select_path - which path is predicted faster for this layer on
  * MI355X (host only): SPCONV_PATH_DENSE when the dense kernel applies (stride
  * 1, 3x3 or 1x1, a plan exists) and the filter density nnz / (K*C*R*S) is
- * above the break-even density measured on MI355X (0.40; the paper's CPU
- * figure is 43.5%); otherwise SPCONV_PATH_SPARSE.
+ * above the break-even density measured on MI355X for the output's size
+ * (0.24 at 14x14, 0.47 at 56x56, log-linear in Ho*Wo between and beyond,
+ * clamped to [0.2, 0.5]; the paper's CPU figure is 43.5%); otherwise
+ * SPCONV_PATH_SPARSE.
  * Errors: SPCONV_EINVAL for a NULL path, sizes < 1, stride < 1, pad < 0, nnz
  * outside [0, K*C*R*S], unknown flags.
  */

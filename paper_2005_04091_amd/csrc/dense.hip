@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 
 #include "common.h"
@@ -59,6 +60,7 @@ struct DenseArgs {
     size_t oplane;
     int res_pad, rpitch;
     size_t rplane;
+    int wpk_bytes;   // bytes of the packed filter (below 2^31)
     int unpadded;    // input is N x C x H x W: the border is formed in LDS
     int H, W, pad, rows_in;
 };
@@ -142,15 +144,23 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
     const int k0 = (kt * a.nw + wn) * kDnsTile;
     const int half = lane >> 5, col = lane & 31;
 
-    f32x16_t acc[NB];
+    // CH independent accumulator chains per pixel block: with one block a
+    // wave's MFMAs would form one dependent chain, so its taps alternate
+    // between two accumulators, added once after the loop.
+    constexpr int CH = NB == 1 ? 2 : 1;
+    f32x16_t acc[NB * CH];
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+    for (int b = 0; b < NB * CH; ++b)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[b][r] = 0.0f;
 
-    // A fragment of (pair cp, tap t): wpk[((cp*RS + t)*Kp + k0 + col)*2 + half].
-    const float *wl = wpk + (size_t)(k0 + col) * 2 + half;
-    const size_t wtap = (size_t)a.Kp * 2;
+    // A fragment of (pair cp, tap t): wpk[((cp*RS + t)*Kp + k0 + col)*2 + half],
+    // read through a buffer descriptor: the lane's part is a fixed VGPR
+    // offset, the (pair, tap) part one scalar offset.
+    const __amdgpu_buffer_rsrc_t wrs =
+        __builtin_amdgcn_make_buffer_rsrc((void *)wpk, (short)0, a.wpk_bytes, 0x00020000);
+    const int wvoff = ((k0 + col) * 2 + half) * (int)sizeof(float);
+    const int wtap_bytes = a.Kp * 2 * (int)sizeof(float);
     // B fragment: the staged channel 2cp + half, pixel 32*b + col, shifted by r*Wp + s.
     const int lane_b = half * a.PLp + col;
 
@@ -173,15 +183,18 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
 #pragma unroll
             for (int s = 0; s < S; ++s) {
                 const float *bt = bp + r * a.Wp + s;
+                const int chain = CH == 2 ? ((r * S + s) & 1) : 0;
 #pragma unroll
                 for (int b = 0; b < NB; ++b)
-                    acc[b] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[r * S + s], bt[kDnsTile * b], acc[b], 0, 0, 0);
+                    acc[b * CH + chain] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[r * S + s], bt[kDnsTile * b],
+                                                                             acc[b * CH + chain], 0, 0, 0);
             }
     };
     auto load_a = [&](float(&av)[RS], int gcp) {
-        const float *wa = wl + (size_t)gcp * RS * wtap;
+        const int base = gcp * RS * wtap_bytes;
 #pragma unroll
-        for (int t = 0; t < RS; ++t) av[t] = wa[t * wtap];
+        for (int t = 0; t < RS; ++t)
+            av[t] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wrs, wvoff, base + t * wtap_bytes, 0));
     };
     for (int ch = 0; ch < a.nchunks; ++ch) {
         if (ch + 1 < a.nchunks) dense_stage(a, xp, lds + ((ch + 1) & 1) * a.buf_floats, ch + 1, n, y0, wave, lane);
@@ -203,6 +216,10 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
         dense_wait_copies();
         __syncthreads();
     }
+
+    if constexpr (CH == 2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[0][r] += acc[1][r];
 
     // Sum the ks partial tiles into the waves with wk == 0, in order wk = 1,
     // 2, ...; the chunk buffers are free after the loop's last barrier.
@@ -445,6 +462,9 @@ int prepare_dense(int N, int C, int H, int W, int K, int R, int S, int pad, uint
     a.C = C;
     a.K = K;
     a.Kp = dense_kp(K);
+    const long long wbytes = (long long)((C + 1) / 2) * R * S * a.Kp * 2 * (long long)sizeof(float);
+    if (wbytes >= (1LL << 31)) return SPCONV_EINVAL;
+    a.wpk_bytes = (int)wbytes;
     a.Hp = (int)Hp;
     a.Wp = (int)Wp;
     a.Ho = Ho;
@@ -539,10 +559,16 @@ namespace {
 
 // Break-even filter density on MI355X: above it the dense kernel beats the
 // sparse ones. Measured with both paths on the same layers (fp32, batch 32):
-// about 0.32 for 256 channels at 14x14 and about 0.45 for 64 channels at
-// 56x56 (where the sparse kernel runs at a higher nonzero rate); one
-// threshold between them, as the paper uses one break-even density.
-constexpr double kBreakEvenDensity = 0.40;
+// about 0.24 for 256 channels at 14x14 and about 0.47 for 64 channels at
+// 56x56. The sparse kernels spread each entry's fixed cost over the pixels
+// of an image tile, so their rate, and the break-even, grow with the image:
+// the threshold interpolates log-linearly in pixels per image between those
+// two measurements, clamped to [0.2, 0.5].
+double break_even_density(int Ho, int Wo) {
+    const double px = std::max(1.0, (double)Ho * Wo);
+    const double d = 0.24 + (0.47 - 0.24) * std::log2(px / 196.0) / std::log2(3136.0 / 196.0);
+    return std::min(0.5, std::max(0.2, d));
+}
 
 }  // namespace
 
@@ -557,6 +583,6 @@ extern "C" int spconv_select_path(int N, int C, int H, int W, int K, int R, int 
     DenseArgs a;
     if (prepare_dense(N, C, H, W, K, R, S, pad, flags & ~SPCONV_UNPADDED_INPUT, nullptr, &pl, &a) != SPCONV_OK)
         return SPCONV_OK;
-    if ((double)nnz > kBreakEvenDensity * (double)K * C * R * S) *path = SPCONV_PATH_DENSE;
+    if ((double)nnz > break_even_density(a.Ho, a.Wo) * (double)K * C * R * S) *path = SPCONV_PATH_DENSE;
     return SPCONV_OK;
 }

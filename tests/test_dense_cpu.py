@@ -110,8 +110,11 @@ def test_select_path(sp):
     assert sel(32, 256, 14, 14, 256, 3, 3, 2, 1, full, 1) == sp.SPCONV_PATH_SPARSE   # stride 2: sparse only
     assert sel(32, 64, 14, 14, 64, 5, 5, 1, 2, 64 * 64 * 25, 1) == sp.SPCONV_PATH_SPARSE  # no 5x5 dense kernel
     assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, 0, 1) == sp.SPCONV_PATH_SPARSE
-    assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.39 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_SPARSE
-    assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.41 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_DENSE
+    # break-even 0.47 at 56x56, 0.24 at 14x14
+    assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.46 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_SPARSE
+    assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.48 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_DENSE
+    assert sel(32, 256, 14, 14, 256, 3, 3, 1, 1, int(0.23 * full), 1) == sp.SPCONV_PATH_SPARSE
+    assert sel(32, 256, 14, 14, 256, 3, 3, 1, 1, int(0.25 * full), 1) == sp.SPCONV_PATH_DENSE
     assert sel(32, 64, 224, 224, 64, 3, 3, 1, 1, 64 * 64 * 9, 3) == sp.SPCONV_PATH_SPARSE  # pooled 226-wide rows: no dense plan
     lib, E, out = sp._lib, sp.SPCONV_EINVAL, ctypes.c_int()
     assert lib.spconv_select_path(32, 64, 56, 56, 64, 3, 3, 1, 1, 7280, 1, None) == E
