@@ -62,15 +62,17 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shi
 // stores. The workgroup's first plane takes one 64-bit division; every quad's
 // plane, row and column inside the workgroup's span take 32-bit
 // multiply-shift divisions.
-constexpr int kPadQuads = 4;
+constexpr int kPadQuads = 2;  // measured on MI355X: 2 beats 1, 4 and 8 (more workgroups in flight)
 constexpr int kPadSpan = 4 * kThreads * kPadQuads;  // elements per workgroup
+constexpr long long kPadMaxPlane = (1LL << 31) - 4096;  // padded planes must stay below this
+static_assert(kPadSpan <= 4096, "a workgroup's span must fit below 2^31 past any plane start");
 
 struct PadArgs {
     const float *in;
     float *out;
     long long total;       // N*C*Hp*Wp
     int H, W, pad, Hp, Wp;
-    int plane;             // Hp*Wp, at most 2^31 - 1 - kPadSpan
+    int plane;             // Hp*Wp, below kPadMaxPlane
     uint32_t plane_magic;  // x / plane == (x * plane_magic) >> plane_shift for 0 <= x < 2^31
     int plane_shift;
     uint32_t wp_magic;     // x / Wp likewise
@@ -1350,7 +1352,7 @@ extern "C" int spconv_pad_input(const float *in, int N, int C, int H, int W, int
     const long long Hp = (long long)H + 2LL * pad, Wp = (long long)W + 2LL * pad;
     const long long plane = Hp * Wp;
     const long long planes = (long long)N * C;
-    if (plane >= (1LL << 31) - kPadSpan || planes * plane >= (1LL << 40)) return SPCONV_EINVAL;
+    if (plane >= kPadMaxPlane || planes * plane >= (1LL << 40)) return SPCONV_EINVAL;
     PadArgs a;
     a.in = in;
     a.out = out_padded;
