@@ -444,7 +444,7 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
         }
         return;
     }
-    const int nblk = a.PLp / kStageBlock;
+    const int nblk = (a.PLp + kStageBlock - 1) / kStageBlock;
     const int plane = a.Hp * a.Wp;
     for (int im = 0; im < a.ipw; ++im) {
         const int nn = ig * a.ipw + im;
@@ -462,8 +462,9 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
         }
         while (cl < cn) {
             const uint32_t voff = (uint32_t)((cl * plane + b * kStageBlock) * (int)sizeof(float)) + lane * 16;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(dst + cl * a.PLp + b * kStageBlock), 16, voff,
-                                                     0, 0, 0);
+            if (b * kStageBlock + lane * 4 < a.PLp)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(dst + cl * a.PLp + b * kStageBlock), 16,
+                                                         voff, 0, 0, 0);
             b += kS1Waves;
             while (b >= nblk) {
                 b -= nblk;
@@ -1186,12 +1187,16 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho
         }
         const int rows_in = TH + R - 1;
         const int PL = rows_in * vp + shift;
-        const int PLp = ceil_div(PL, kStageBlock) * kStageBlock;
+        // Channel slots 16-byte aligned; a slot's last copy masks the lanes
+        // past it (rounding slots up to whole 256-float copies would cost
+        // LDS and, at 64 channels of 56x56, a fourth chunk).
+        const int PLp = ceil_div(PL, 4) * 4;
         // Lanes past the tile read up to cap - TH*vp + S - 2 floats beyond the
-        // last image block; keep that inside the buffer.
+        // last image block (values that only dropped pixels use). Past the
+        // first buffer they land in the second; past the second, in one slack
+        // area after it.
         const int slack = cap - TH * vp + S;
-        const int per_buf = kS1LdsFloats / 2;
-        int cc_max = (per_buf - slack) / (IPW * PLp);
+        int cc_max = ((kS1LdsFloats - slack) / 2) / (IPW * PLp);
         if (cc_max < 1) return;
         cc_max = std::min(cc_max, C);
         const int nchunks = ceil_div(C, cc_max);
@@ -1222,12 +1227,12 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho
             best.PL = PL;
             best.PLp = PLp;
             best.img_lds = Cc * PLp;
-            best.buf_floats = ceil_div(IPW * Cc * PLp + slack, 64) * 64;
+            best.buf_floats = ceil_div(IPW * Cc * PLp, 64) * 64;
             best.wv = vp;
             best.rows_per_wg = KT;
             best.nktiles = ceil_div(K, KT);
             best.total_wgs = (int)wgs;
-            size_t floats = 2 * (size_t)best.buf_floats;
+            size_t floats = 2 * (size_t)best.buf_floats + slack;
             if (pool) floats = std::max(floats, (size_t)kS1Waves * IPW * kWave * PI);
             best.lds_bytes = floats * sizeof(float);
         }

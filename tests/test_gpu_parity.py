@@ -266,10 +266,10 @@ VARIANTS = [
     ("ipw4_rpw2_ragged_n", 31, 3, 520, 2, False, False, (2, 4, 2)),
     ("ipw4_rpw4", 64, 3, 520, 2, False, False, (2, 4, 4)),
     ("ipw4_rpw4_pool", 64, 3, 520, 2, True, False, (2, 4, 4)),
-    ("ipw2_rpw2_chunks_overflow", 16, 200, 520, 2, False, True, (2, 2, 2)),
-    ("ipw2_rpw1_chunks", 32, 200, 520, 2, False, False, (2, 2, 1)),
-    ("ipw1_rpw4_chunks_overflow", 16, 100, 520, 12, False, True, (4, 1, 4)),
-    ("ipw1_rpw2_pool_chunks_overflow", 8, 100, 520, 12, True, True, (4, 1, 2)),
+    ("ipw2_rpw2_chunks_overflow", 16, 700, 520, 2, False, True, (2, 2, 2)),
+    ("ipw2_rpw1_chunks", 32, 700, 520, 2, False, False, (2, 2, 1)),
+    ("ipw1_rpw4_chunks_overflow", 16, 250, 520, 12, False, True, (4, 1, 4)),
+    ("ipw1_rpw2_pool_chunks_overflow", 8, 250, 520, 12, True, True, (4, 1, 2)),
     ("ipw4_rpw1_pool", 16, 3, 520, 2, True, False, (2, 4, 1)),
     ("ipw4_rpw2_pool", 32, 3, 520, 2, True, False, (2, 4, 2)),
 ]
@@ -284,6 +284,8 @@ def test_kernel_variant(sp, case):
     plan = L.plan(N)
     say("variant", name, layer.shape, plan)
     assert (plan["pixels_per_lane"], plan["images_per_group"], plan["channels_per_wave"]) == expect
+    if "chunks" in name:
+        assert plan["chunks"] >= 2, "the variant must span several LDS chunks"
     out = L.run(torch.from_numpy(layer.x).cuda())
     torch.cuda.synchronize()
     ref, ab = oracle_layer(layer)
