@@ -637,6 +637,25 @@ __device__ __forceinline__ void merge_pairs(const float2 (&e)[PJ], const float2 
     }
 }
 
+// Issue priority (0 lowest .. 3 highest) from a wave's progress through its
+// entries of the current chunk. Among ready waves of equal priority a SIMD
+// issues the oldest first, so left alone the oldest wave of each SIMD runs
+// ahead, the youngest finishes every chunk alone at a fraction of the SIMD's
+// rate, and the others idle at the chunk barrier. Dropping one level per
+// quarter of the chunk done lets the waves that are behind issue first, and
+// the four waves of a SIMD reach the barrier nearly together.
+__device__ __forceinline__ void set_progress_prio(int done, int total) {
+    const int d4 = 4 * done;
+    if (d4 >= 3 * total)
+        __builtin_amdgcn_s_setprio(0);
+    else if (d4 >= 2 * total)
+        __builtin_amdgcn_s_setprio(1);
+    else if (d4 >= total)
+        __builtin_amdgcn_s_setprio(2);
+    else
+        __builtin_amdgcn_s_setprio(3);
+}
+
 template <int PI, int IPW, int RPW, bool POOL>
 __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4))) void spconv_s1_kernel(
     FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ offset,
@@ -735,13 +754,21 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
         }
         const int bound = bound_of(ch);
         const int vb = vb_of(ch);
+        int total = 0, done = 0;
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) total += win[i].n;
+        set_progress_prio(0, total);
 #pragma unroll
         for (int i = 0; i < RPW; ++i) {
             for (;;) {
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
                     run_mask(accE[i], win[i].lo[h], win[i].w[h], win[i].even[h], lds, q, a.img_lds);
+                    done += __builtin_popcountll(win[i].even[h]);
+                    set_progress_prio(done, total);
                     run_mask(accO[i], win[i].lo[h], win[i].w[h], win[i].odd[h], lds, q, a.img_lds);
+                    done += __builtin_popcountll(win[i].odd[h]);
+                    set_progress_prio(done, total);
                 }
                 const int n = win[i].n;
                 cur[i] += n;
@@ -1208,6 +1235,11 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho
         if (wgs > 0x7fffffffLL) return;
         const double pair_skew = 1.0 + (skew - 1.0) / (2.0 * RPW - 1.0);
         const double imb = std::max(1.0, (RPW == 1 ? skew : pair_skew) / 1.3) * (RPW == 1 ? 1.03 : 1.0);
+        // Buffers rounded up to 64 floats may not fit once slack is added.
+        const int buf_floats = ceil_div(IPW * Cc * PLp, 64) * 64;
+        size_t floats = 2 * (size_t)buf_floats + slack;
+        if (pool) floats = std::max(floats, (size_t)kS1Waves * IPW * kWave * PI);
+        if (floats > (size_t)kS1LdsFloats) return;
         const double compute = kS1Waves * RPW * row_nnz * 2.0 * (IPW * PI + 1.0) * imb;
         const double wg_cycles =
             compute + nchunks * (3000.0 + IPW * (double)Cc * PLp / 32.0) + (pool ? 4000.0 * RPW : 0.0);
@@ -1227,13 +1259,11 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho
             best.PL = PL;
             best.PLp = PLp;
             best.img_lds = Cc * PLp;
-            best.buf_floats = ceil_div(IPW * Cc * PLp, 64) * 64;
+            best.buf_floats = buf_floats;
             best.wv = vp;
             best.rows_per_wg = KT;
             best.nktiles = ceil_div(K, KT);
             best.total_wgs = (int)wgs;
-            size_t floats = 2 * (size_t)best.buf_floats + slack;
-            if (pool) floats = std::max(floats, (size_t)kS1Waves * IPW * kWave * PI);
             best.lds_bytes = floats * sizeof(float);
         }
     };
