@@ -33,6 +33,17 @@ __device__ __forceinline__ void store_out(float *p, float v, bool stream) {
         *p = v;
 }
 
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two adjacent output elements, p 8-byte aligned; streaming as store_out.
+__device__ __forceinline__ void store_out2(float *p, float2 v, bool stream) {
+    const f32x2_t t = {v.x, v.y};
+    if (stream)
+        __builtin_nontemporal_store(t, reinterpret_cast<f32x2_t *>(p));
+    else
+        *reinterpret_cast<f32x2_t *>(p) = t;
+}
+
 __device__ __forceinline__ void stream_store4(float *p, float4 v) {
     const f32x4_t t = {v.x, v.y, v.z, v.w};
     __builtin_nontemporal_store(t, reinterpret_cast<f32x4_t *>(p));

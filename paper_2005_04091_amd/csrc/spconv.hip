@@ -347,6 +347,10 @@ struct FwdArgs {
     int vp, lds_shift, dma16;
     uint32_t wp_magic;  // x / Wp == (x * wp_magic) >> wp_shift
     int wp_shift;
+    // stride-1 unpooled epilogue: a lane's pixel pair (2l, 2l+1) always lies in
+    // one stored row or outside the output, and its output (and residual)
+    // elements are 8-byte aligned, so each pair moves with one 8-byte access
+    int pair_store;
 };
 
 // Queue asynchronous global->LDS copies of one channel chunk: for each image of
@@ -825,6 +829,25 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
                         : nullptr;
                 float2 sum[PJ];
                 merge_pairs(accE[i][im], accO[i][im], sum, lane);
+                if (a.pair_store) {
+#pragma unroll
+                    for (int p = 0; p < PJ; ++p) {
+                        const int yl = ylo[p][0];
+                        if (yl < 0) continue;
+                        const int qq = q + 2 * kWave * p;
+                        float2 v = make_float2(sum[p].x + bk, sum[p].y + bk);
+                        if (rp) {
+                            const float2 r = *reinterpret_cast<const float2 *>(rp + qq + yl * rdelta);
+                            v.x += r.x;
+                            v.y += r.y;
+                        }
+                        if (a.relu) {
+                            v.x = v.x > 0.0f ? v.x : 0.0f;
+                            v.y = v.y > 0.0f ? v.y : 0.0f;
+                        }
+                        store_out2(op + qq + yl * odelta, v, a.out_pad == 0);
+                    }
+                } else {
 #pragma unroll
                 for (int p = 0; p < PJ; ++p)
 #pragma unroll
@@ -837,6 +860,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
                         if (a.relu) v = v > 0.0f ? v : 0.0f;
                         store_out(op + qq + yl * odelta, v, a.out_pad == 0);
                     }
+                }
                 if (a.out_pad)
                     zero_border(plane, y0, min(y0 + a.TH, a.Ho), a.Ho, a.Wo, a.out_pad, a.opitch, ty == 0,
                                 ty == a.ntiles_y - 1, lane, kWave);
@@ -1514,6 +1538,7 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.vp = pl.kind == Kind::kStride1 ? pl.wv : (int)Wp;
     a.lds_shift = row16 ? (4 - pad % 4) % 4 : 0;
     a.dma16 = row16 ? 1 : 0;
+    a.pair_store = 0;
     if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift)) return SPCONV_EINVAL;
     a.H = H;
     a.W = W;
@@ -1594,6 +1619,12 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
     // 16-byte row copies need a 16-byte aligned tensor; otherwise the same
     // layout is filled 4 bytes per lane.
     if (a.dma16 && (reinterpret_cast<uintptr_t>(in_padded) & 15) != 0) a.dma16 = 0;
+    // Pixel pairs (2l, 2l+1) of the virtual tile share a row when its pitch vp
+    // is even, and are both inside or both outside the output when Wo is even
+    // too; with even pitches and borders their elements start at even indices.
+    a.pair_store = pl.kind == Kind::kStride1 && (flags & SPCONV_MAXPOOL2X2) == 0 && a.vp % 2 == 0 &&
+                   a.Wo % 2 == 0 && a.out_pad % 2 == 0 && (reinterpret_cast<uintptr_t>(out) & 7) == 0 &&
+                   (!residual || (a.res_pad % 2 == 0 && (reinterpret_cast<uintptr_t>(residual) & 7) == 0));
     FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0);
     const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
     if (pl.lds_bytes > 65536 &&

@@ -80,7 +80,7 @@ def test_out_pad_matches_plain_call_bitwise(sp, i, out_pad):
     assert np.array_equal(got.view(np.uint32), ref.view(np.uint32)), "padded output differs from pad(plain output)"
 
 
-@pytest.mark.parametrize("res_pad", [0, 1])
+@pytest.mark.parametrize("res_pad", [0, 1, 2])
 @pytest.mark.parametrize("i", range(len(CASES)))
 def test_residual_against_oracle(sp, i, res_pad):
     import torch
@@ -98,6 +98,37 @@ def test_residual_against_oracle(sp, i, res_pad):
     ref, ab = oracle.conv(layer.x, layer.w, layer.mask, layer.bias, layer.stride, layer.pad, layer.relu, layer.pool,
                           residual=res)
     check_close(out.cpu().numpy(), ref, ab, f"residual {CASES[i]}")
+
+
+@pytest.mark.parametrize("i", [0, 2, 7])
+def test_misaligned_output_and_residual_match_aligned_bitwise(sp, i):
+    """Output and residual tensors that start 4 bytes past an 8-byte boundary
+    are stored and read one element at a time; tensors at 8-byte boundaries
+    (even widths) move a lane's pixel pair with one 8-byte access. Both give
+    the same bits."""
+    import torch
+    layer = _layer(i, CASES[i])
+    N, C, H, W, K, R, S = layer.shape
+    L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, layer.stride, layer.pad, layer.relu, layer.pool)
+    Ho, Wo = L.Ho, L.Wo
+    say("misaligned out/residual", CASES[i], L.plan(N))
+    xp = L.pad_input(torch.from_numpy(layer.x).cuda())
+    res = np.random.default_rng(300 + i).uniform(-1, 1, (N, K, Ho, Wo)).astype(np.float32)
+    n = res.size
+    res_a = torch.from_numpy(res).cuda()
+    res_base = torch.empty(n + 1, device="cuda")
+    res_m = res_base[1:].view(N, K, Ho, Wo)
+    res_m.copy_(res_a)
+    out_a = torch.full((N, K, Ho, Wo), float("nan"), device="cuda")
+    out_base = torch.full((n + 1,), float("nan"), device="cuda")
+    out_m = out_base[1:].view(N, K, Ho, Wo)
+    assert out_a.data_ptr() % 8 == 0 and out_m.data_ptr() % 8 == 4 and res_m.data_ptr() % 8 == 4
+    for res_dev in (None, res_a, res_m):
+        kw = {} if res_dev is None else dict(residual=res_dev, residual_pad=0)
+        L.forward_padded(xp, out=out_a, **kw)
+        L.forward_padded(xp, out=out_m, **kw)
+        torch.cuda.synchronize()
+        assert np.array_equal(out_a.cpu().numpy().view(np.uint32), out_m.cpu().numpy().view(np.uint32))
 
 
 def test_residual_and_out_pad_together(sp):
