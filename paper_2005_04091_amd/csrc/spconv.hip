@@ -578,47 +578,61 @@ __device__ __forceinline__ float lane_read_f(float v, int l) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
-// Accumulate the window entries whose lanes are set in mask m into acc. Two-
-// stage software pipeline: the LDS reads of the next entry are in flight
-// while the FMAs of the current one issue; the entries are visited in lane
-// order through the mask's set bits (scalar find-first-set). The loop body
-// has no exit in the middle, so the accumulators stay in place.
-template <int PJ, int IPW>
+// Accumulate the window entries whose lanes are set in mask m into acc, in
+// lane order (scalar find-first-set over the mask). Software pipeline of NB
+// buffers: the LDS reads of the next NB-1 entries are in flight while the
+// FMAs of the current one issue. Each entry's reads then have NB-1 entries'
+// worth of this wave's FMAs to arrive; tilings with few pixels per lane (few
+// FMAs per entry) need the deeper pipelines. Buffer indices are compile-time
+// constants in the unrolled bodies, so the buffers stay in registers; the
+// scheduling barriers keep each refill after the FMAs that read the buffer it
+// overwrites. The main loop has no exit in the middle, so the accumulators
+// stay in place.
+template <int NB, int PJ, int IPW>
 __device__ __forceinline__ void run_mask(float2 (&acc)[IPW][PJ], int lo, float w, uint64_t m, const float *lds,
                                          int q, int img_lds) {
-    int n = __builtin_popcountll(m);
-    if (n == 0) return;
-    f32x2 x0[IPW][PJ], x1[IPW][PJ];
-    int u0 = __builtin_ctzll(m);
-    m &= m - 1;
-    load_pairs(x0, lds, lane_read_i(lo, u0) + q, img_lds);
-    float w0 = lane_read_f(w, u0);
-    // The scheduling barriers keep each refill after the FMAs that read the
-    // buffer it overwrites, so the two buffers alternate without copies.
-    for (; n > 2; n -= 2) {
-        const int u1 = __builtin_ctzll(m);
+    int r = __builtin_popcountll(m);
+    if (r == 0) return;
+    f32x2 x[NB][IPW][PJ];
+    float wt[NB];
+    auto next = [&](f32x2 (&xb)[IPW][PJ], float &wb) {
+        const int u = __builtin_ctzll(m);
         m &= m - 1;
-        const float w1 = lane_read_f(w, u1);
-        load_pairs(x1, lds, lane_read_i(lo, u1) + q, img_lds);
-        fma_pairs(acc, x0, w0);
-        __builtin_amdgcn_sched_barrier(0);
-        u0 = __builtin_ctzll(m);
-        m &= m - 1;
-        w0 = lane_read_f(w, u0);
-        load_pairs(x0, lds, lane_read_i(lo, u0) + q, img_lds);
-        fma_pairs(acc, x1, w1);
+        wb = lane_read_f(w, u);
+        load_pairs(xb, lds, lane_read_i(lo, u) + q, img_lds);
+    };
+#pragma unroll
+    for (int b = 0; b < NB - 1; ++b)
+        if (b < r) next(x[b], wt[b]);
+    // Invariant: buffers 0..NB-2 hold the next NB-1 entries; an iteration
+    // loads the NB after them, so at least 2*NB - 1 must remain.
+    for (; r >= 2 * NB - 1; r -= NB) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            next(x[(b + NB - 1) % NB], wt[(b + NB - 1) % NB]);
+            fma_pairs(acc, x[b], wt[b]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < 2 * NB - 2; ++b) {
+        if (b >= r) break;
+        if (b + NB - 1 < r) next(x[(b + NB - 1) % NB], wt[(b + NB - 1) % NB]);
+        fma_pairs(acc, x[b % NB], wt[b % NB]);
         __builtin_amdgcn_sched_barrier(0);
     }
-    if (n == 2) {
-        const int u1 = __builtin_ctzll(m);
-        const float w1 = lane_read_f(w, u1);
-        load_pairs(x1, lds, lane_read_i(lo, u1) + q, img_lds);
-        fma_pairs(acc, x0, w0);
-        __builtin_amdgcn_sched_barrier(0);
-        fma_pairs(acc, x1, w1);
-    } else {
-        fma_pairs(acc, x0, w0);
-    }
+}
+
+// Pipeline depth of the stride-1 kernel: deeper for fewer FMAs per entry
+// (IPW * PI), where the 128 VGPRs of four waves per SIMD hold the buffers
+// (accumulators plus buffers within 98 floats, at most two channels a wave:
+// each channel's window state takes registers too).
+template <int PI, int IPW, int RPW>
+constexpr int pipeline_buffers() {
+    const int want = IPW * PI <= 8 ? 3 : 2;
+    for (int nb = want; nb > 2; --nb)
+        if (RPW <= 2 && 2 * RPW * IPW * PI + nb * IPW * PI <= 98) return nb;
+    return 2;
 }
 
 // Sums of this lane's virtual pixel pairs (2l + 128j, 2l+1 + 128j) of one
@@ -767,10 +781,12 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
             for (;;) {
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
-                    run_mask(accE[i], win[i].lo[h], win[i].w[h], win[i].even[h], lds, q, a.img_lds);
+                    run_mask<pipeline_buffers<PI, IPW, RPW>()>(accE[i], win[i].lo[h], win[i].w[h], win[i].even[h],
+                                                               lds, q, a.img_lds);
                     done += __builtin_popcountll(win[i].even[h]);
                     set_progress_prio(done, total);
-                    run_mask(accO[i], win[i].lo[h], win[i].w[h], win[i].odd[h], lds, q, a.img_lds);
+                    run_mask<pipeline_buffers<PI, IPW, RPW>()>(accO[i], win[i].lo[h], win[i].w[h], win[i].odd[h],
+                                                               lds, q, a.img_lds);
                     done += __builtin_popcountll(win[i].odd[h]);
                     set_progress_prio(done, total);
                 }
