@@ -35,6 +35,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <type_traits>
 
 #include "common.h"
 #include "spconv.h"
@@ -501,22 +502,43 @@ __device__ __forceinline__ RawWindow fetch_window(const int32_t *__restrict__ of
     return r;
 }
 
-// A window decoded for one channel chunk: per slot, the LDS float index of
-// each entry's tap for virtual pixel 0 rounded down to even (`lo`), its
-// weight, and two lane masks that split the entries of the chunk (a prefix of
-// the window) by the parity of that index; `n` counts them. Even taps are read
-// as aligned pixel pairs (2l, 2l+1); odd taps as the aligned pairs (2l-1, 2l),
-// which accumulate into the pixel-shifted accumulator set.
-struct Window {
+// A window decoded for one channel chunk. Per slot, the entries of the chunk
+// (a prefix of the window) are split by the parity of their tap's LDS float
+// index for virtual pixel 0; each lane holds that index rounded down to even
+// (`lo`) and its weight. Even taps are read as aligned pixel pairs (2l, 2l+1);
+// odd taps as the aligned pairs (2l-1, 2l), which accumulate into the
+// pixel-shifted accumulator set. Two forms:
+//  * masks: the entries stay in their lanes; `even`/`odd` are the lane masks
+//    of the two classes, walked with find-first-set;
+//  * compacted: lanes 0..ne-1 hold the even taps, ne..ne+no-1 the odd ones
+//    (CSR order within each class), walked with a counter: three fewer
+//    scalar instructions per entry, which pays where an entry has few FMAs.
+// `n` counts the chunk's entries. (Each form holds only its own fields: the
+// scalar registers of two channels' windows are a tight budget.)
+struct WindowMasks {
     int lo[2];
     float w[2];
     uint64_t even[2], odd[2];
     int n;
 };
+struct WindowCompact {
+    int lo[2];
+    float w[2];
+    int ne[2], no[2];
+    int n;
+};
+template <bool COMPACT>
+using Window = typename std::conditional<COMPACT, WindowCompact, WindowMasks>::type;
 
-__device__ __forceinline__ Window decode_window(const FwdArgs &a, const RawWindow &r, int e, int bound, int vb,
-                                                int lane) {
-    Window win;
+// Number of set bits of m in lanes below this one.
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+template <bool COMPACT>
+__device__ __forceinline__ Window<COMPACT> decode_window(const FwdArgs &a, const RawWindow &r, int e, int bound,
+                                                         int vb, int lane) {
+    Window<COMPACT> win;
     win.n = 0;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -528,16 +550,30 @@ __device__ __forceinline__ Window decode_window(const FwdArgs &a, const RawWindo
         const int tap_row = (int)fast_div((uint32_t)(o - c * a.Hp * a.Wp), a.wp_magic, a.wp_shift);
         const int t = vb + o - c * a.plane_delta + tap_row * (a.vp - a.Wp) + a.lds_shift;
         const int odd = t & 1;
-        win.lo[h] = t - odd;
-        // Touch the loaded weight here, so that the wait for its load is
-        // placed at this decode and not deferred into the compute loop, where
-        // it would also wait for the chunk copies in flight.
-        float w = r.w[h];
-        asm volatile("" : "+v"(w));
-        win.w[h] = w;
-        win.even[h] = __builtin_amdgcn_ballot_w64(in && !odd);
-        win.odd[h] = __builtin_amdgcn_ballot_w64(in && odd);
-        win.n += __builtin_popcountll(win.even[h] | win.odd[h]);
+        const uint64_t me = __builtin_amdgcn_ballot_w64(in && !odd);
+        const uint64_t mo = __builtin_amdgcn_ballot_w64(in && odd);
+        const int ne = __builtin_popcountll(me), no = __builtin_popcountll(mo);
+        if constexpr (COMPACT) {
+            // Destination lane: even taps first, then odd ones, then the lanes
+            // outside the chunk (a permutation of the 64 lanes).
+            const int be = lanes_below(me), bo = ne + lanes_below(mo), bx = ne + no + lanes_below(~(me | mo));
+            const int dst = in ? (odd ? bo : be) : bx;
+            win.lo[h] = __builtin_amdgcn_ds_permute(dst * 4, t - odd);
+            win.w[h] = __int_as_float(__builtin_amdgcn_ds_permute(dst * 4, __float_as_int(r.w[h])));
+            win.ne[h] = ne;
+            win.no[h] = no;
+        } else {
+            win.lo[h] = t - odd;
+            // Touch the loaded weight here, so that the wait for its load is
+            // placed at this decode and not deferred into the compute loop,
+            // where it would also wait for the chunk copies in flight.
+            float w = r.w[h];
+            asm volatile("" : "+v"(w));
+            win.w[h] = w;
+            win.even[h] = me;
+            win.odd[h] = mo;
+        }
+        win.n += ne + no;
     }
     return win;
 }
@@ -579,15 +615,7 @@ __device__ __forceinline__ float lane_read_f(float v, int l) {
 }
 
 // Accumulate the window entries whose lanes are set in mask m into acc, in
-// lane order (scalar find-first-set over the mask). Software pipeline of NB
-// buffers: the LDS reads of the next NB-1 entries are in flight while the
-// FMAs of the current one issue. Each entry's reads then have NB-1 entries'
-// worth of this wave's FMAs to arrive; tilings with few pixels per lane (few
-// FMAs per entry) need the deeper pipelines. Buffer indices are compile-time
-// constants in the unrolled bodies, so the buffers stay in registers; the
-// scheduling barriers keep each refill after the FMAs that read the buffer it
-// overwrites. The main loop has no exit in the middle, so the accumulators
-// stay in place.
+// lane order (scalar find-first-set); the same pipeline as run_range below.
 template <int NB, int PJ, int IPW>
 __device__ __forceinline__ void run_mask(float2 (&acc)[IPW][PJ], int lo, float w, uint64_t m, const float *lds,
                                          int q, int img_lds) {
@@ -600,6 +628,47 @@ __device__ __forceinline__ void run_mask(float2 (&acc)[IPW][PJ], int lo, float w
         m &= m - 1;
         wb = lane_read_f(w, u);
         load_pairs(xb, lds, lane_read_i(lo, u) + q, img_lds);
+    };
+#pragma unroll
+    for (int b = 0; b < NB - 1; ++b)
+        if (b < r) next(x[b], wt[b]);
+    for (; r >= 2 * NB - 1; r -= NB) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            next(x[(b + NB - 1) % NB], wt[(b + NB - 1) % NB]);
+            fma_pairs(acc, x[b], wt[b]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+#pragma unroll
+    for (int b = 0; b < 2 * NB - 2; ++b) {
+        if (b >= r) break;
+        if (b + NB - 1 < r) next(x[(b + NB - 1) % NB], wt[(b + NB - 1) % NB]);
+        fma_pairs(acc, x[b % NB], wt[b % NB]);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+// Accumulate window entries j0..j1-1 (compacted lanes) into acc. Software
+// pipeline of NB buffers: the LDS reads of the next NB-1 entries are in
+// flight while the FMAs of the current one issue. Each entry's reads then
+// have NB-1 entries' worth of this wave's FMAs to arrive; tilings with few
+// pixels per lane (few FMAs per entry) need the deeper pipelines. Buffer
+// indices are compile-time constants in the unrolled bodies, so the buffers
+// stay in registers; the scheduling barriers keep each refill after the FMAs
+// that read the buffer it overwrites. The main loop has no exit in the
+// middle, so the accumulators stay in place.
+template <int NB, int PJ, int IPW>
+__device__ __forceinline__ void run_range(float2 (&acc)[IPW][PJ], int lo, float w, int j, int j1, const float *lds,
+                                          int q, int img_lds) {
+    int r = j1 - j;
+    if (r <= 0) return;
+    f32x2 x[NB][IPW][PJ];
+    float wt[NB];
+    auto next = [&](f32x2 (&xb)[IPW][PJ], float &wb) {
+        wb = lane_read_f(w, j);
+        load_pairs(xb, lds, lane_read_i(lo, j) + q, img_lds);
+        ++j;
     };
 #pragma unroll
     for (int b = 0; b < NB - 1; ++b)
@@ -683,6 +752,8 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
     constexpr int KT = RPW * kS1Waves;  // output channels per workgroup
     constexpr int PJ = PI / 2;          // pixel pairs per lane per image
     static_assert(PI % 2 == 0, "pixels per lane come in pairs");
+    constexpr int NB = pipeline_buffers<PI, IPW, RPW>();
+    constexpr bool kCompact = NB > 2;  // compacted windows where entries have few FMAs
 
     const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
@@ -743,7 +814,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
     auto bound_of = [&](int ch) { return min((ch + 1) * a.Cc, a.C) * plane; };
     const int q = 2 * lane;
 
-    Window win[RPW];
+    Window<kCompact> win[RPW];
     RawWindow next[RPW];
     if (a.unpadded) {
         // Zero both chunk buffers once: the staging of an unpadded input never
@@ -756,7 +827,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
         next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
-        win[i] = decode_window(a, next[i], end[i], bound_of(0), vb_of(0), lane);
+        win[i] = decode_window<kCompact>(a, next[i], end[i], bound_of(0), vb_of(0), lane);
     }
     wait_async_copies();
     __syncthreads();
@@ -781,20 +852,28 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
             for (;;) {
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
-                    run_mask<pipeline_buffers<PI, IPW, RPW>()>(accE[i], win[i].lo[h], win[i].w[h], win[i].even[h],
-                                                               lds, q, a.img_lds);
-                    done += __builtin_popcountll(win[i].even[h]);
-                    set_progress_prio(done, total);
-                    run_mask<pipeline_buffers<PI, IPW, RPW>()>(accO[i], win[i].lo[h], win[i].w[h], win[i].odd[h],
-                                                               lds, q, a.img_lds);
-                    done += __builtin_popcountll(win[i].odd[h]);
+                    if constexpr (kCompact) {
+                        const int ne = win[i].ne[h], no = win[i].no[h];
+                        run_range<NB>(accE[i], win[i].lo[h], win[i].w[h], 0, ne, lds, q, a.img_lds);
+                        done += ne;
+                        set_progress_prio(done, total);
+                        run_range<NB>(accO[i], win[i].lo[h], win[i].w[h], ne, ne + no, lds, q, a.img_lds);
+                        done += no;
+                    } else {
+                        run_mask<NB>(accE[i], win[i].lo[h], win[i].w[h], win[i].even[h], lds, q, a.img_lds);
+                        done += __builtin_popcountll(win[i].even[h]);
+                        set_progress_prio(done, total);
+                        run_mask<NB>(accO[i], win[i].lo[h], win[i].w[h], win[i].odd[h], lds, q, a.img_lds);
+                        done += __builtin_popcountll(win[i].odd[h]);
+                    }
                     set_progress_prio(done, total);
                 }
                 const int n = win[i].n;
                 cur[i] += n;
                 if (n < 2 * kWave || cur[i] >= end[i]) break;
                 // The row has more entries in this chunk than one window holds.
-                win[i] = decode_window(a, fetch_window(offset, vals, cur[i], end[i], lane), end[i], bound, vb, lane);
+                win[i] = decode_window<kCompact>(a, fetch_window(offset, vals, cur[i], end[i], lane), end[i], bound,
+                                                 vb, lane);
             }
         }
         if (more) {
@@ -802,7 +881,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
             for (int i = 0; i < RPW; ++i) {
                 // A row that overflowed a window in this chunk ends elsewhere.
                 if (next[i].base != cur[i]) next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
-                win[i] = decode_window(a, next[i], end[i], bound_of(ch + 1), vb_of(ch + 1), lane);
+                win[i] = decode_window<kCompact>(a, next[i], end[i], bound_of(ch + 1), vb_of(ch + 1), lane);
             }
         }
         // Chunk ch+1 is in LDS and every wave is done with chunk ch's buffer.
