@@ -38,7 +38,7 @@ constexpr int kDnsTile = 32;              // MFMA tile: 32 channels x 32 pixels
 constexpr int kDnsMaxWaves = 4;           // channel tiles (of 32) per workgroup
 constexpr int kDnsMaxThreads = 512;       // nw * ks waves per workgroup, at most 8
 constexpr int kDnsMaxBlocks = 8;          // pixel blocks per wave (16 accumulator VGPRs each)
-constexpr int kDnsCopy = 64;              // floats per one-dword-per-lane LDS DMA instruction
+constexpr int kDnsBlock = 256;            // floats per 16-byte-per-lane LDS DMA instruction
 constexpr int kDnsLdsBytes = 64 * 1024;   // per workgroup: two resident per CU
 constexpr int kDnsPoolCh = 8;             // channels of one pooled staging round (4 accumulator rows x 2 halves)
 
@@ -66,16 +66,18 @@ struct DenseArgs {
 };
 
 // Queue the copy of one channel chunk of the tile: channel cl of the chunk gets
-// PLp floats from the tile's first padded row at buf + cl*PLp. Each unit is one
-// dword per lane; units are dealt round-robin to the waves. Copies past the
-// channel's rows read the next rows (never used by a stored pixel); the buffer
-// range stops them at the end of the input tensor (such lanes read 0).
+// PLp floats from the tile's first padded row at buf + cl*PLp. A unit (channel,
+// block of 256 floats) is one 16-byte-per-lane copy; units are dealt round-
+// robin to the waves (the LDS-DMA engine's cost is per instruction, so 1 KiB
+// copies move four times the bytes of dword ones for the same cost); the last
+// block of a channel masks the lanes past PLp. Copies past the channel's rows
+// read the next rows (never used by a stored pixel); the buffer range stops
+// them at the end of the input tensor (such lanes read 0).
 __device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__restrict__ xp, float *buf, int ch,
                                             int n, int row0, int wave, int lane) {
     const int c0 = ch * a.Cc;
     const int cn = min(a.Cc, a.C - c0);
-    const int nblk = a.PLp / kDnsCopy;
-    const size_t plane = (size_t)a.Hp * a.Wp;
+    const int plane = a.Hp * a.Wp;
     const int nwaves = a.nw * a.ks;
     if (a.unpadded) {
         // Row by row from the unpadded input: padded row row0 + i is image row
@@ -107,14 +109,30 @@ __device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__r
             }
         }
     }
-    for (int u = wave; !a.unpadded && u < cn * nblk; u += nwaves) {
-        const int cl = u / nblk, b = u - cl * nblk;
-        const size_t first = ((size_t)n * a.C + c0 + cl) * plane + (size_t)row0 * a.Wp + (size_t)b * kDnsCopy;
+    if (!a.unpadded) {
+        const int nblk = (a.PLp + kDnsBlock - 1) / kDnsBlock;
+        const size_t first = ((size_t)n * a.C + c0) * plane + (size_t)row0 * a.Wp;
         const size_t avail = (a.total_floats - first) * sizeof(float);
         const int nrec = avail > 0xffffffffull ? (int)0xffffffffu : (int)(uint32_t)avail;
-        __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void *)(xp + first), (short)0, nrec, 0x00020000);
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(buf + cl * a.PLp + b * kDnsCopy), 4, lane * 4, 0,
-                                                 0, 0);
+        __amdgpu_buffer_rsrc_t rsrc =
+            __builtin_amdgcn_make_buffer_rsrc((void *)(xp + first), (short)0, nrec, 0x00020000);
+        int cl = 0, b = wave;
+        while (b >= nblk) {
+            b -= nblk;
+            ++cl;
+        }
+        while (cl < cn) {
+            // Byte offsets of a chunk fit 32 bits (the planner checks).
+            const uint32_t voff = (uint32_t)(cl * plane + b * kDnsBlock) * (uint32_t)sizeof(float) + lane * 16;
+            if (b * kDnsBlock + lane * 4 < a.PLp)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(buf + cl * a.PLp + b * kDnsBlock), 16,
+                                                         voff, 0, 0, 0);
+            b += nwaves;
+            while (b >= nblk) {
+                b -= nblk;
+                ++cl;
+            }
+        }
     }
     // An odd last chunk reads one channel slot past the tensor's channels with
     // zero weights; it must hold finite values: zero it.
@@ -412,11 +430,14 @@ bool plan_dense(int N, int C, int K, int Wp, int Ho, int R, int S, bool pool, De
     p.ntiles_y = (Ho + p.TH - 1) / p.TH;
     // A channel's staged rows must cover every B read: the last block's last
     // pixel shifted by the largest tap offset.
-    p.PLp = round_up(std::max((p.TH + R - 1) * Wp, p.NB * kDnsTile + (R - 1) * Wp + S - 1), kDnsCopy);
+    // Slots are 16-byte aligned for the 16-byte copies.
+    p.PLp = round_up(std::max((p.TH + R - 1) * Wp, p.NB * kDnsTile + (R - 1) * Wp + S - 1), 4);
     const int cmax = kDnsLdsBytes / (2 * p.PLp * (int)sizeof(float)) / 2 * 2;
     if (cmax < 2) return false;
     p.Cc = std::min(cmax, round_up(C, 2));
     p.nchunks = (C + p.Cc - 1) / p.Cc;
+    // The copy offsets of one chunk are 32-bit byte offsets (and int floats).
+    if (((long long)(p.Cc - 1) * (Ho + R - 1) * Wp + p.PLp + kDnsBlock) * 4 >= (1LL << 31)) return false;
     // Split the reduction over more waves (2 or 4 per channel tile) while the
     // grid has fewer than 4 waves per SIMD, within 8 waves per workgroup and
     // an LDS area of 64 KiB for summing the partial tiles.
