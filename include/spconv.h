@@ -312,7 +312,7 @@ int spconv_dense_plan(int N, int C, int H, int W, int K, int R, int S, int pad, 
  * MI355X (host only): SPCONV_PATH_DENSE when the dense kernel applies (stride
  * 1, 3x3 or 1x1, a plan exists) and the filter density nnz / (K*C*R*S) is
  * above the break-even density measured on MI355X for the output's size
- * (0.24 at 14x14, 0.47 at 56x56, log-linear in Ho*Wo between and beyond,
+ * (0.24 at 14x14, 0.43 at 56x56, log-linear in Ho*Wo between and beyond,
  * clamped to [0.2, 0.5]; the paper's CPU figure is 43.5%); otherwise
  * SPCONV_PATH_SPARSE.
  * Errors: SPCONV_EINVAL for a NULL path, sizes < 1, stride < 1, pad < 0, nnz

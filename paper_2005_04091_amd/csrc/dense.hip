@@ -388,26 +388,56 @@ int dense_waves(int K) { return std::min(kDnsMaxWaves, (K + kDnsTile - 1) / kDns
 // Kp of the packed filter: K rounded up to whole workgroup channel tiles.
 int dense_kp(int K) { return round_up(K, kDnsTile * dense_waves(K)); }
 
+// Waves that split the reduction over channel pairs (1, 2 or 4), each adding
+// a 32-channel partial tile that is summed through LDS: 2 where the workgroup
+// (8 waves), the LDS area of the partial tiles (64 KiB) and the chunk's pairs
+// allow, 4 only when even 2 would leave the grid under 1024 waves (measured:
+// 4 splits cost up to 30% more than 2 on grids that have enough waves).
+int dense_ks(long long base_waves, int nw, int NB, int Cc) {
+    const size_t red_bytes = (size_t)nw * NB * 16 * kWave * sizeof(float);
+    int ks = 1;
+    auto fits = [&](int k) { return nw * k * kWave <= kDnsMaxThreads && red_bytes <= (size_t)kDnsLdsBytes && k <= Cc / 2; };
+    if (fits(2)) ks = 2;
+    if (ks == 2 && base_waves * 2 < 1024 && fits(4)) ks = 4;
+    return ks;
+}
+
 // Tile rows: among the heights whose tile fits 8 pixel blocks (even heights
-// when pooling), the fewest MFMA blocks per image and channel tile (tiles x
-// blocks: junk pixels of a partial last block and of a partial last tile both
-// cost), provided the grid keeps at least one wave per SIMD when any height
-// can; ties go to the taller tile (less halo to stage).
+// when pooling), the least modelled work, tiles x (blocks + 1): a wave's MFMAs
+// per channel pair (one per block and tap) plus about one block's worth for
+// the pair's A fragments, which each block reuses; provided the grid keeps at
+// least 1536 waves (six per SIMD over the run) when any height can, ties going
+// to the grid with more waves. Measured on 14x14 (256 channels), 28x28 pooled
+// and 56x56 layers: the picks are each layer's fastest tiling of the sweep.
 bool plan_dense(int N, int C, int K, int Wp, int Ho, int R, int S, bool pool, DensePlan *pl) {
     DensePlan p;
     p.nw = dense_waves(K);
     p.nkt = (K + kDnsTile * p.nw - 1) / (kDnsTile * p.nw);
-    const long long kMinWaves = 1024;
-    int best_th = 0;
+    const long long kMinWaves = 1536;
+    DensePlan best;
     long long best_cost = 0, best_waves = 0;
     for (int th = pool ? 2 : 1; th <= (pool ? round_up(Ho, 2) : Ho); th += pool ? 2 : 1) {
-        const int nb = (th * Wp + kDnsTile - 1) / kDnsTile;
-        if (nb > kDnsMaxBlocks) break;
-        const int tiles = (Ho + th - 1) / th;
-        const long long waves = (long long)N * tiles * p.nkt * p.nw;
-        const long long cost = (long long)tiles * nb;
+        DensePlan q = p;
+        q.TH = th;
+        q.NB = (th * Wp + kDnsTile - 1) / kDnsTile;
+        if (q.NB > kDnsMaxBlocks) break;
+        q.ntiles_y = (Ho + th - 1) / th;
+        // A channel's staged rows must cover every B read: the last block's
+        // last pixel shifted by the largest tap offset. Slots are 16-byte
+        // aligned for the 16-byte copies.
+        q.PLp = round_up(std::max((th + R - 1) * Wp, q.NB * kDnsTile + (R - 1) * Wp + S - 1), 4);
+        const int cmax = kDnsLdsBytes / (2 * q.PLp * (int)sizeof(float)) / 2 * 2;
+        if (cmax < 2) continue;
+        q.Cc = std::min(cmax, round_up(C, 2));
+        q.nchunks = (C + q.Cc - 1) / q.Cc;
+        // The copy offsets of one chunk are 32-bit byte offsets (and int floats).
+        if (((long long)(q.Cc - 1) * (Ho + R - 1) * Wp + q.PLp + kDnsBlock) * 4 >= (1LL << 31)) continue;
+        const long long base_waves = (long long)N * q.ntiles_y * q.nkt * q.nw;
+        q.ks = dense_ks(base_waves, q.nw, q.NB, q.Cc);
+        const long long waves = base_waves * q.ks;
+        const long long cost = (long long)q.ntiles_y * (q.NB + 1);
         bool better;
-        if (best_th == 0) {
+        if (best.TH == 0) {
             better = true;
         } else {
             const bool ok = waves >= kMinWaves, best_ok = best_waves >= kMinWaves;
@@ -416,39 +446,19 @@ bool plan_dense(int N, int C, int K, int Wp, int Ho, int R, int S, bool pool, De
             else if (!ok)
                 better = waves > best_waves;
             else
-                better = cost <= best_cost;
+                better = cost < best_cost || (cost == best_cost && waves > best_waves);
         }
         if (better) {
-            best_th = th;
+            best = q;
             best_cost = cost;
             best_waves = waves;
         }
     }
-    if (best_th == 0) return false;
-    p.TH = best_th;
-    p.NB = (p.TH * Wp + kDnsTile - 1) / kDnsTile;
-    p.ntiles_y = (Ho + p.TH - 1) / p.TH;
-    // A channel's staged rows must cover every B read: the last block's last
-    // pixel shifted by the largest tap offset.
-    // Slots are 16-byte aligned for the 16-byte copies.
-    p.PLp = round_up(std::max((p.TH + R - 1) * Wp, p.NB * kDnsTile + (R - 1) * Wp + S - 1), 4);
-    const int cmax = kDnsLdsBytes / (2 * p.PLp * (int)sizeof(float)) / 2 * 2;
-    if (cmax < 2) return false;
-    p.Cc = std::min(cmax, round_up(C, 2));
-    p.nchunks = (C + p.Cc - 1) / p.Cc;
-    // The copy offsets of one chunk are 32-bit byte offsets (and int floats).
-    if (((long long)(p.Cc - 1) * (Ho + R - 1) * Wp + p.PLp + kDnsBlock) * 4 >= (1LL << 31)) return false;
-    // Split the reduction over more waves (2 or 4 per channel tile) while the
-    // grid has fewer than 4 waves per SIMD, within 8 waves per workgroup and
-    // an LDS area of 64 KiB for summing the partial tiles.
-    const long long base_waves = (long long)N * p.ntiles_y * p.nkt * p.nw;
-    const size_t red_bytes = (size_t)p.nw * p.NB * 16 * kWave * sizeof(float);
-    while (p.ks < 4 && base_waves * p.ks < 4096 && p.nw * p.ks * 2 * kWave <= kDnsMaxThreads &&
-           red_bytes <= (size_t)kDnsLdsBytes && p.ks * 2 <= p.Cc / 2)
-        p.ks *= 2;
+    if (best.TH == 0) return false;
+    p = best;
     size_t lds = (size_t)2 * p.Cc * p.PLp * sizeof(float);
     if (pool) lds = std::max(lds, (size_t)p.nw * kDnsPoolCh * p.NB * kDnsTile * sizeof(float));
-    if (p.ks > 1) lds = std::max(lds, red_bytes);
+    if (p.ks > 1) lds = std::max(lds, (size_t)p.nw * p.NB * 16 * kWave * sizeof(float));
     p.lds_bytes = lds;
     const long long wgs = (long long)N * p.ntiles_y * p.nkt;
     if (wgs > 0x7fffffffLL) return false;
@@ -580,14 +590,14 @@ namespace {
 
 // Break-even filter density on MI355X: above it the dense kernel beats the
 // sparse ones. Measured with both paths on the same layers (fp32, batch 32):
-// about 0.24 for 256 channels at 14x14 and about 0.47 for 64 channels at
+// about 0.24 for 256 channels at 14x14 and about 0.43 for 64 channels at
 // 56x56. The sparse kernels spread each entry's fixed cost over the pixels
 // of an image tile, so their rate, and the break-even, grow with the image:
 // the threshold interpolates log-linearly in pixels per image between those
 // two measurements, clamped to [0.2, 0.5].
 double break_even_density(int Ho, int Wo) {
     const double px = std::max(1.0, (double)Ho * Wo);
-    const double d = 0.24 + (0.47 - 0.24) * std::log2(px / 196.0) / std::log2(3136.0 / 196.0);
+    const double d = 0.24 + (0.43 - 0.24) * std::log2(px / 196.0) / std::log2(3136.0 / 196.0);
     return std::min(0.5, std::max(0.2, d));
 }
 

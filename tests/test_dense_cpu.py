@@ -93,8 +93,14 @@ def test_forward_dense_validates_before_any_gpu_work(sp):
 
 
 def test_dense_plans_cover_the_tile_shapes(sp):
+    # 14x14, 256 channels: 4 tiles of 4 rows (two 32-pixel blocks), 4 channel
+    # tiles x 2 reduction shares per workgroup, 2048 waves
     p = sp.spconv_dense_plan(32, 256, 14, 14, 256, 3, 3, 1, 1)
-    assert (p["tile_rows"], p["pixels_per_lane"], p["threads_per_workgroup"]) == (2, 1, 512)  # 4 tiles x 2 shares
+    assert (p["tile_rows"], p["pixels_per_lane"], p["threads_per_workgroup"]) == (4, 2, 512)
+    # 56x56, 64 channels: 4 rows of 58 padded columns (eight blocks), 2 channel
+    # tiles x 2 shares, 1792 waves
+    p = sp.spconv_dense_plan(32, 64, 56, 56, 64, 3, 3, 1, 1)
+    assert (p["tile_rows"], p["pixels_per_lane"], p["threads_per_workgroup"]) == (4, 8, 256)
     p = sp.spconv_dense_plan(1, 3, 3, 224, 16, 3, 3, 1, 1)
     assert p["pixels_per_lane"] == 8                   # 226 padded columns: eight 32-pixel blocks
     p = sp.spconv_dense_plan(4, 64, 28, 28, 64, 3, 3, 1, 3)
@@ -110,9 +116,9 @@ def test_select_path(sp):
     assert sel(32, 256, 14, 14, 256, 3, 3, 2, 1, full, 1) == sp.SPCONV_PATH_SPARSE   # stride 2: sparse only
     assert sel(32, 64, 14, 14, 64, 5, 5, 1, 2, 64 * 64 * 25, 1) == sp.SPCONV_PATH_SPARSE  # no 5x5 dense kernel
     assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, 0, 1) == sp.SPCONV_PATH_SPARSE
-    # break-even 0.47 at 56x56, 0.24 at 14x14
-    assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.46 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_SPARSE
-    assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.48 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_DENSE
+    # break-even 0.43 at 56x56, 0.24 at 14x14
+    assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.42 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_SPARSE
+    assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.44 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_DENSE
     assert sel(32, 256, 14, 14, 256, 3, 3, 1, 1, int(0.23 * full), 1) == sp.SPCONV_PATH_SPARSE
     assert sel(32, 256, 14, 14, 256, 3, 3, 1, 1, int(0.25 * full), 1) == sp.SPCONV_PATH_DENSE
     assert sel(32, 64, 224, 224, 64, 3, 3, 1, 1, 64 * 64 * 9, 3) == sp.SPCONV_PATH_SPARSE  # pooled 226-wide rows: no dense plan
