@@ -193,7 +193,10 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
 
     // Two A register sets alternate over this wave's pairs (wk, wk + ks, ...)
     // of each chunk: the loads for the next pair are in flight while the MFMAs
-    // of the current one issue.
+    // of the current one issue. With few blocks a pair's MFMAs are short next
+    // to an A load's latency (an L2 hit), and a third set keeps two pairs'
+    // loads in flight.
+    constexpr bool kA3 = NB <= 4;
     auto mma_pair = [&](const float(&av)[RS], int cp, const float *bb) {
         const float *bp = bb + 2 * cp * a.PLp;
 #pragma unroll
@@ -220,15 +223,33 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
         const int c0 = ch * a.Cc;
         const int npairs = (min(a.Cc, a.C - c0) + 1) / 2;
         const int gcp0 = c0 / 2;
-        float a0[RS], a1[RS];
-        if (wk < npairs) load_a(a0, gcp0 + wk);
-        for (int cp = wk; cp < npairs; cp += 2 * a.ks) {
-            const int cq = cp + a.ks;
-            if (cq < npairs) load_a(a1, gcp0 + cq);
-            mma_pair(a0, cp, bb);
-            if (cq < npairs) {
-                if (cq + a.ks < npairs) load_a(a0, gcp0 + cq + a.ks);
-                mma_pair(a1, cq, bb);
+        if constexpr (kA3) {
+            // Three A sets: the loads of the next two pairs are in flight.
+            float a0[RS], a1[RS], a2[RS];
+            const int st = a.ks;
+            if (wk < npairs) load_a(a0, gcp0 + wk);
+            if (wk + st < npairs) load_a(a1, gcp0 + wk + st);
+            for (int cp = wk; cp < npairs; cp += 3 * st) {
+                if (cp + 2 * st < npairs) load_a(a2, gcp0 + cp + 2 * st);
+                mma_pair(a0, cp, bb);
+                if (cp + st >= npairs) break;
+                if (cp + 3 * st < npairs) load_a(a0, gcp0 + cp + 3 * st);
+                mma_pair(a1, cp + st, bb);
+                if (cp + 2 * st >= npairs) break;
+                if (cp + 4 * st < npairs) load_a(a1, gcp0 + cp + 4 * st);
+                mma_pair(a2, cp + 2 * st, bb);
+            }
+        } else {
+            float a0[RS], a1[RS];
+            if (wk < npairs) load_a(a0, gcp0 + wk);
+            for (int cp = wk; cp < npairs; cp += 2 * a.ks) {
+                const int cq = cp + a.ks;
+                if (cq < npairs) load_a(a1, gcp0 + cq);
+                mma_pair(a0, cp, bb);
+                if (cq < npairs) {
+                    if (cq + a.ks < npairs) load_a(a0, gcp0 + cq + a.ks);
+                    mma_pair(a1, cq, bb);
+                }
             }
         }
         dense_wait_copies();
