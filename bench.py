@@ -204,6 +204,9 @@ def cpu_baseline(layer, budget_s: float, nthreads: int = 0):
     return {"value": flops / dt / 1e9, "unit": "GFLOP/s", "cores": threads, "kind": "oracle", "sample": sample}
 
 
+BLOCK_ROUNDS = 5
+
+
 def bench_block(args, dev):
     """A chained block per step, with inputs resident in HBM: layer 1 forms its
     input's zero border in the kernel when its rows are wide enough (else one
@@ -270,10 +273,16 @@ def bench_block(args, dev):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / args.steps
 
-    ms = timed(fused)
-    ms_chained = timed(chained_out_pad)
-    ms_in_kernel = timed(all_in_kernel)
-    ms_unfused = timed(unfused)
+    # The variants are timed in rounds, in rotating order, and each reports
+    # its median round: whichever runs first after the others would otherwise
+    # carry the clock and cache state they leave behind.
+    variants = [fused, chained_out_pad, all_in_kernel, unfused]
+    times = [[] for _ in variants]
+    for r in range(BLOCK_ROUNDS):
+        for i in range(len(variants)):
+            j = (i + r) % len(variants)
+            times[j].append(timed(variants[j]))
+    ms, ms_chained, ms_in_kernel, ms_unfused = (statistics.median(t) for t in times)
     nnz1, nnz2 = L1.host_csr.nnz, L2.host_csr.nnz
     flops = 2.0 * (nnz1 + nnz2) * N * H * W
     rec = {
@@ -296,6 +305,7 @@ def bench_block(args, dev):
         "ms_per_step_both_pad_in_kernel": round(ms_in_kernel, 5),
         "layer1_pads_in_kernel": l1_in_kernel,
         "fusion_saving_frac": round(1.0 - ms / ms_unfused, 4),
+        "timing": f"median of {BLOCK_ROUNDS} rounds of {args.steps} steps per variant, variants in rotating order",
     }
     print(json.dumps(rec), flush=True)
 
@@ -347,9 +357,13 @@ def bench_resize_block(args, dev):
     def resize_only():
         L.resize_pad_input(sd, out=xp, stream=stream)
 
-    ms = _timed(args, stream, fused)
-    ms_unfused = _timed(args, stream, unfused)
-    ms_resize = _timed(args, stream, resize_only)
+    variants = [fused, unfused, resize_only]
+    times = [[] for _ in variants]
+    for r in range(BLOCK_ROUNDS):
+        for i in range(len(variants)):
+            j = (i + r) % len(variants)
+            times[j].append(_timed(args, stream, variants[j]))
+    ms, ms_unfused, ms_resize = (statistics.median(t) for t in times)
     nnz = L.host_csr.nnz
     flops = 2.0 * nnz * N * H * W
     rbytes = resize_source_bytes(N * C, Hin, Win, H, W) + 4.0 * N * C * (H + 2) * (W + 2)
@@ -370,6 +384,7 @@ def bench_resize_block(args, dev):
                    "W": W, "nnz": nnz, "pool": True},
         "ms_per_step_unfused": round(ms_unfused, 5),
         "fusion_saving_frac": round(1.0 - ms / ms_unfused, 4),
+        "timing": f"median of {BLOCK_ROUNDS} rounds of {args.steps} steps per variant, variants in rotating order",
         "resize_kernel": {"ms": round(ms_resize, 5), "algorithmic_bytes": rbytes,
                           "GB/s": round(rbytes / (ms_resize * 1e-3) / 1e9, 1),
                           "hbm_frac": round(rbytes / (ms_resize * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},

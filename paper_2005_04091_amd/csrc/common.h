@@ -33,15 +33,17 @@ __device__ __forceinline__ void store_out(float *p, float v, bool stream) {
         *p = v;
 }
 
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
+// Two adjacent floats at any 4-byte boundary: gfx9 global loads and stores of
+// two dwords need only dword alignment.
+typedef float f32x2_a4_t __attribute__((ext_vector_type(2), aligned(4)));
 
-// Two adjacent output elements, p 8-byte aligned; streaming as store_out.
+// Two adjacent output elements (p 4-byte aligned); streaming as store_out.
 __device__ __forceinline__ void store_out2(float *p, float2 v, bool stream) {
-    const f32x2_t t = {v.x, v.y};
+    const f32x2_a4_t t = {v.x, v.y};
     if (stream)
-        __builtin_nontemporal_store(t, reinterpret_cast<f32x2_t *>(p));
+        __builtin_nontemporal_store(t, reinterpret_cast<f32x2_a4_t *>(p));
     else
-        *reinterpret_cast<f32x2_t *>(p) = t;
+        *reinterpret_cast<f32x2_a4_t *>(p) = t;
 }
 
 __device__ __forceinline__ void stream_store4(float *p, float4 v) {

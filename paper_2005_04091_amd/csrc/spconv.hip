@@ -349,8 +349,8 @@ struct FwdArgs {
     uint32_t wp_magic;  // x / Wp == (x * wp_magic) >> wp_shift
     int wp_shift;
     // stride-1 unpooled epilogue: a lane's pixel pair (2l, 2l+1) always lies in
-    // one stored row or outside the output, and its output (and residual)
-    // elements are 8-byte aligned, so each pair moves with one 8-byte access
+    // one stored row or outside the output, so each pair moves with one
+    // two-dword access
     int pair_store;
 };
 
@@ -932,7 +932,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
                         const int qq = q + 2 * kWave * p;
                         float2 v = make_float2(sum[p].x + bk, sum[p].y + bk);
                         if (rp) {
-                            const float2 r = *reinterpret_cast<const float2 *>(rp + qq + yl * rdelta);
+                            const f32x2_a4_t r = *reinterpret_cast<const f32x2_a4_t *>(rp + qq + yl * rdelta);
                             v.x += r.x;
                             v.y += r.y;
                         }
@@ -1716,10 +1716,10 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
     if (a.dma16 && (reinterpret_cast<uintptr_t>(in_padded) & 15) != 0) a.dma16 = 0;
     // Pixel pairs (2l, 2l+1) of the virtual tile share a row when its pitch vp
     // is even, and are both inside or both outside the output when Wo is even
-    // too; with even pitches and borders their elements start at even indices.
+    // too; two-dword accesses need only 4-byte aligned tensors.
     a.pair_store = pl.kind == Kind::kStride1 && (flags & SPCONV_MAXPOOL2X2) == 0 && a.vp % 2 == 0 &&
-                   a.Wo % 2 == 0 && a.out_pad % 2 == 0 && (reinterpret_cast<uintptr_t>(out) & 7) == 0 &&
-                   (!residual || (a.res_pad % 2 == 0 && (reinterpret_cast<uintptr_t>(residual) & 7) == 0));
+                   a.Wo % 2 == 0 && (reinterpret_cast<uintptr_t>(out) & 3) == 0 &&
+                   (!residual || (reinterpret_cast<uintptr_t>(residual) & 3) == 0);
     FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0);
     const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
     if (pl.lds_bytes > 65536 &&

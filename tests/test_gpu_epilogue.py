@@ -103,9 +103,9 @@ def test_residual_against_oracle(sp, i, res_pad):
 @pytest.mark.parametrize("i", [0, 2, 7])
 def test_misaligned_output_and_residual_match_aligned_bitwise(sp, i):
     """Output and residual tensors that start 4 bytes past an 8-byte boundary
-    are stored and read one element at a time; tensors at 8-byte boundaries
-    (even widths) move a lane's pixel pair with one 8-byte access. Both give
-    the same bits."""
+    give the same bits as aligned ones (with even widths a lane's pixel pair
+    moves with one two-dword access, which needs only 4-byte alignment; odd
+    widths store element by element)."""
     import torch
     layer = _layer(i, CASES[i])
     N, C, H, W, K, R, S = layer.shape
