@@ -348,6 +348,11 @@ struct FwdArgs {
     int vp, lds_shift, dma16;
     uint32_t wp_magic;  // x / Wp == (x * wp_magic) >> wp_shift
     int wp_shift;
+    // stride-1 epilogues: x / vp, x / ((TH/2) * Wq) and x / Wq as multiply-
+    // shift (a runtime integer division is some 30 instructions, several of
+    // them quarter rate, per stored pixel)
+    uint32_t vp_magic, pimg_magic, wq_magic;
+    int vp_shift, pimg_shift, wq_shift;
     // stride-1 unpooled epilogue: a lane's pixel pair (2l, 2l+1) always lies in
     // one stored row or outside the output, so each pair moves with one
     // two-dword access
@@ -904,7 +909,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int qq = q + 2 * kWave * p + h;
-                const int yl = qq / a.vp, x = qq - yl * a.vp;
+                const int yl = (int)fast_div((uint32_t)qq, a.vp_magic, a.vp_shift), x = qq - yl * a.vp;
                 ylo[p][h] = (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) ? yl : -1;
             }
         const int odelta = a.opitch - a.vp, rdelta = a.rpitch - a.vp;
@@ -994,7 +999,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 #pragma unroll
                         for (int h = 0; h < 2; ++h) {
                             const int qq = q + 2 * kWave * p + h;
-                            const int yl = qq / a.vp, x = qq - yl * a.vp;
+                            const int yl = (int)fast_div((uint32_t)qq, a.vp_magic, a.vp_shift), x = qq - yl * a.vp;
                             if (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) v[h] += rp[qq + yl * (a.rpitch - a.vp)];
                         }
                     }
@@ -1008,9 +1013,9 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the whole tile is staged
             if (k < a.K) {
                 for (int t = lane; t < IPW * per_img; t += kWave) {
-                    const int im = t / per_img;
+                    const int im = (int)fast_div((uint32_t)t, a.pimg_magic, a.pimg_shift);
                     const int rem = t - im * per_img;
-                    const int r = rem / a.Wq;
+                    const int r = (int)fast_div((uint32_t)rem, a.wq_magic, a.wq_shift);
                     const int jq = rem - r * a.Wq;
                     const int n = ig * IPW + im;
                     const int pr = prow0 + r;
@@ -1635,6 +1640,7 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.dma16 = row16 ? 1 : 0;
     a.pair_store = 0;
     if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift)) return SPCONV_EINVAL;
+    if (!div_magic((uint32_t)a.vp, &a.vp_magic, &a.vp_shift)) return SPCONV_EINVAL;
     a.H = H;
     a.W = W;
     a.pad = pad;
@@ -1647,6 +1653,12 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.Wo = Wo;
     a.Hq = pool ? Ho / 2 : Ho;
     a.Wq = pool ? Wo / 2 : Wo;
+    a.pimg_magic = a.wq_magic = 1;
+    a.pimg_shift = a.wq_shift = 0;
+    if (pl.kind == Kind::kStride1 && pool &&
+        (!div_magic((uint32_t)((pl.TH / 2) * a.Wq), &a.pimg_magic, &a.pimg_shift) ||
+         !div_magic((uint32_t)a.Wq, &a.wq_magic, &a.wq_shift)))
+        return SPCONV_EINVAL;
     a.stride = stride;
     a.nnz = (int)csr->nnz;
     a.relu = (flags & SPCONV_RELU) ? 1 : 0;
