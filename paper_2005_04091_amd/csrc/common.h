@@ -51,6 +51,29 @@ __device__ __forceinline__ void stream_store4(float *p, float4 v) {
     __builtin_nontemporal_store(t, reinterpret_cast<f32x4_t *>(p));
 }
 
+// x / d for x < 2^31 as one multiply-high and a shift, with (magic, shift)
+// from div_magic(d) on the host (round-up reciprocal, shift 31 + ceil(log2 d)).
+__device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shift) {
+    return (uint32_t)(((uint64_t)x * (uint64_t)magic) >> shift);
+}
+
+inline bool div_magic(uint32_t d, uint32_t *magic, int *shift) {
+    if (d == 0) return false;
+    if (d == 1) {
+        *magic = 1;
+        *shift = 0;
+        return true;
+    }
+    int L = 0;
+    while ((1ull << L) < d) ++L;
+    const int s = 31 + L;
+    const uint64_t m = ((1ull << s) + d - 1) / d;
+    if (m > 0xffffffffull) return false;
+    *magic = (uint32_t)m;
+    *shift = s;
+    return true;
+}
+
 // Workgroup id -> linear work index such that consecutive work items (the
 // channel tiles of one image tile, which read the same input rows) land on the
 // same XCD and therefore share its L2.

@@ -61,6 +61,9 @@ struct DenseArgs {
     int res_pad, rpitch;
     size_t rplane;
     int wpk_bytes;   // bytes of the packed filter (below 2^31)
+    // epilogues: x / Wp, x / ((TH/2) * Wq) and x / Wq as multiply-shift
+    uint32_t wp_magic, pch_magic, wq_magic;
+    int wp_shift, pch_shift, wq_shift;
     int unpadded;    // input is N x C x H x W: the border is formed in LDS
     int H, W, pad, rows_in;
 };
@@ -286,6 +289,16 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
     const int tile_px = a.TH * a.Wp;
     const bool stream = a.out_pad == 0;
     if constexpr (!POOL) {
+        // Row and column of this lane's pixel in each block (-1: not stored).
+        int ys[NB], xs[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int q = kDnsTile * b + col;
+            const int yl = (int)fast_div((uint32_t)q, a.wp_magic, a.wp_shift), x = q - yl * a.Wp;
+            const bool in = q < tile_px && x < a.Wo && y0 + yl < a.Ho;
+            ys[b] = in ? y0 + yl : -1;
+            xs[b] = x;
+        }
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const int k = k0 + 8 * (j >> 2) + 4 * half + (j & 3);
@@ -295,10 +308,8 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
             const float *rplane = res ? res + ((size_t)n * a.K + k) * a.rplane : nullptr;
 #pragma unroll
             for (int b = 0; b < NB; ++b) {
-                const int q = kDnsTile * b + col;
-                const int yl = q / a.Wp, x = q - yl * a.Wp;
-                const int y = y0 + yl;
-                if (q >= tile_px || x >= a.Wo || y >= a.Ho) continue;
+                const int y = ys[b], x = xs[b];
+                if (y < 0) continue;
                 float v = acc[b][j] + bk;
                 if (rplane) v += rplane[(size_t)(y + a.res_pad) * a.rpitch + x + a.res_pad];
                 if (a.relu) v = v > 0.0f ? v : 0.0f;
@@ -335,7 +346,7 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
                     const int q = kDnsTile * b + col;
                     float v = acc[b][j] + bk;
                     if (rplane) {
-                        const int yl = q / a.Wp, x = q - yl * a.Wp;
+                        const int yl = (int)fast_div((uint32_t)q, a.wp_magic, a.wp_shift), x = q - yl * a.Wp;
                         if (q < tile_px && x < a.Wo && y0 + yl < a.Ho)
                             v += rplane[(size_t)(y0 + yl + a.res_pad) * a.rpitch + x + a.res_pad];
                     }
@@ -345,9 +356,9 @@ __global__ __launch_bounds__(kDnsMaxThreads) void spconv_dense_kernel(DenseArgs 
             }
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             for (int t = lane; t < kDnsPoolCh * per_ch; t += kWave) {
-                const int cc = t / per_ch;
+                const int cc = (int)fast_div((uint32_t)t, a.pch_magic, a.pch_shift);
                 const int rem = t - cc * per_ch;
-                const int r = rem / a.Wq, jq = rem - r * a.Wq;
+                const int r = (int)fast_div((uint32_t)rem, a.wq_magic, a.wq_shift), jq = rem - r * a.Wq;
                 const int k = k0 + 8 * g + cc;
                 const int pr = prow0 + r;
                 if (k < a.K && pr < a.Hq) {
@@ -523,6 +534,12 @@ int prepare_dense(int N, int C, int H, int W, int K, int R, int S, int pad, uint
     a.Wo = Wo;
     a.Hq = pool ? Ho / 2 : Ho;
     a.Wq = pool ? Wo / 2 : Wo;
+    a.pch_magic = a.wq_magic = 1;
+    a.pch_shift = a.wq_shift = 0;
+    if (!div_magic((uint32_t)a.Wp, &a.wp_magic, &a.wp_shift) ||
+        (pool && (!div_magic((uint32_t)((pl.TH / 2) * a.Wq), &a.pch_magic, &a.pch_shift) ||
+                  !div_magic((uint32_t)a.Wq, &a.wq_magic, &a.wq_shift))))
+        return SPCONV_EINVAL;
     a.relu = (flags & SPCONV_RELU) ? 1 : 0;
     a.unpadded = (flags & SPCONV_UNPADDED_INPUT) ? 1 : 0;
     a.H = H;

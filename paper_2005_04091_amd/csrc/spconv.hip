@@ -46,9 +46,6 @@ constexpr int kWaves = 4;
 constexpr int kThreads = kWave * kWaves;
 constexpr int kLdsBudgetFloats = 20480;   // generic kernel: 80 KiB of LDS per workgroup (two per CU)
 
-__device__ __forceinline__ uint32_t fast_div(uint32_t x, uint32_t magic, int shift) {
-    return (uint32_t)(((uint64_t)x * (uint64_t)magic) >> shift);
-}
 
 // ---------------------------------------------------------------------------
 // Padded input (spconv_pad_input)
@@ -1220,23 +1217,6 @@ __global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, con
 // x / d == (x * magic) >> shift for all 0 <= x < 2^31 (d >= 1): with
 // L = ceil(log2 d), magic = ceil(2^(31+L) / d) < 2^32 and the rounding error
 // x * (magic*d - 2^(31+L)) / (d * 2^(31+L)) stays below 1/d.
-bool div_magic(uint32_t d, uint32_t *magic, int *shift) {
-    if (d == 0) return false;
-    if (d == 1) {
-        *magic = 1;
-        *shift = 0;
-        return true;
-    }
-    int L = 0;
-    while ((1ull << L) < d) ++L;
-    const int s = 31 + L;
-    const uint64_t m = ((1ull << s) + d - 1) / d;
-    if (m > 0xffffffffull) return false;
-    *magic = (uint32_t)m;
-    *shift = s;
-    return true;
-}
-
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 enum class Kind { kStride1, kGeneric };
