@@ -256,3 +256,36 @@ def test_plan_reports_the_launch_without_a_gpu(sp):
     assert plan(2, 5, 9, 8, 7, flags=8)[0] == sp.SPCONV_EINVAL
     csr = sp.spconv_csr(7, 5, 3, 3, 11, 10, 60, fake, fake, fake, fake, 0)
     assert lib.spconv_plan(2, 5, 9, 8, ctypes.byref(csr), 7, 3, 3, 1, 1, 1, None) == sp.SPCONV_EINVAL
+
+
+def test_plans_fit_the_lds_over_a_sweep_of_shapes(sp):
+    """Every stride-1 plan fits one CU's 160 KiB of LDS (chunk buffers rounded to
+    64 floats, the slack after them, the pooled staging area), and every dense
+    plan its 64 KiB, over widths, heights, channel counts, batch sizes and
+    pooling; the grid covers each (image group, tile, channel tile) once."""
+    lib = sp._lib
+    fake = 0x1000
+    seen = seen_dense = 0
+    for N in (1, 3, 32):
+        for C in (1, 3, 16, 64, 130, 512):
+            for H, W in ((2, 2), (7, 9), (14, 14), (28, 28), (56, 56), (61, 70), (224, 224), (5, 600)):
+                for pool in (False, True):
+                    flags = sp.SPCONV_RELU | (sp.SPCONV_MAXPOOL2X2 if pool else 0)
+                    K = 64
+                    nnz = max(1, int(0.2 * K * C * 9))
+                    csr = sp.spconv_csr(K, C, 3, 3, H + 2, W + 2, nnz, fake, fake, fake, fake, 0)
+                    info = sp.spconv_plan_info()
+                    rc = lib.spconv_plan(N, C, H, W, ctypes.byref(csr), K, 3, 3, 1, 1, flags, ctypes.byref(info))
+                    if rc != sp.SPCONV_OK:
+                        continue
+                    seen += 1
+                    assert 0 < info.lds_bytes <= 160 * 1024, (N, C, H, W, pool, info.lds_bytes)
+                    if info.kernel == sp.SPCONV_KERNEL_STRIDE1:
+                        kt = 16 * info.channels_per_wave
+                        assert info.workgroups == -(-N // info.images_per_group) * info.tiles_per_image * -(-K // kt)
+                        assert info.channels_per_chunk * info.chunks >= C
+                    dinfo = sp.spconv_plan_info()
+                    if lib.spconv_dense_plan(N, C, H, W, K, 3, 3, 1, flags, ctypes.byref(dinfo)) == sp.SPCONV_OK:
+                        seen_dense += 1
+                        assert 0 < dinfo.lds_bytes <= 64 * 1024, (N, C, H, W, pool, dinfo.lds_bytes)
+    assert seen > 200 and seen_dense > 100
