@@ -1346,7 +1346,7 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho
         if (floats > (size_t)kS1LdsFloats) return;
         const double compute = kS1Waves * RPW * row_nnz * 2.0 * (IPW * PI + 1.0) * imb;
         const double wg_cycles =
-            compute + nchunks * (3000.0 + IPW * (double)Cc * PLp / 32.0) + (pool ? 4000.0 * RPW : 0.0);
+            compute + nchunks * (3000.0 + IPW * (double)Cc * PLp / 32.0) + (pool ? 8000.0 * RPW : 0.0);
         const double time = (double)ceil_div((int)std::min<long long>(wgs, 1 << 30), 256) * wg_cycles;
         if (best_time < 0 || time < best_time * 0.999) {
             best_time = time;

@@ -256,16 +256,16 @@ def test_vgg_block_chain_full_size(sp):
 VARIANTS = [
     # name, N, C, K, H(=W), pool, skewed rows, expected (PI, IPW, RPW)
     ("ipw1_rpw2", 8, 3, 520, 12, False, True, (4, 1, 2)),
-    ("ipw1_rpw2_pool", 8, 8, 520, 12, True, True, (4, 1, 2)),
+    ("ipw1_rpw2_pool", 4, 16, 1040, 12, True, True, (4, 1, 2)),
     ("ipw1_rpw4", 16, 3, 520, 12, False, True, (4, 1, 4)),
     ("ipw2_rpw1", 8, 3, 520, 2, False, False, (2, 2, 1)),
     ("ipw2_rpw1_pool", 8, 3, 520, 2, True, False, (2, 2, 1)),
     ("ipw2_rpw2", 16, 3, 520, 2, False, True, (2, 2, 2)),
-    ("ipw2_rpw2_pool", 16, 8, 520, 2, True, True, (2, 2, 2)),
+    ("ipw2_rpw2_pool", 8, 16, 1040, 2, True, True, (2, 2, 2)),
     ("ipw2_rpw4", 32, 3, 520, 2, False, True, (2, 2, 4)),
     ("ipw4_rpw2_ragged_n", 31, 3, 520, 2, False, False, (2, 4, 2)),
     ("ipw4_rpw4", 64, 3, 520, 2, False, False, (2, 4, 4)),
-    ("ipw4_rpw4_pool", 64, 3, 520, 2, True, False, (2, 4, 4)),
+    ("ipw4_rpw4_pool", 32, 3, 1040, 2, True, True, (2, 4, 4)),
     ("ipw2_rpw2_chunks_overflow", 16, 700, 520, 2, False, True, (2, 2, 2)),
     ("ipw2_rpw1_chunks", 32, 700, 520, 2, False, False, (2, 2, 1)),
     ("ipw1_rpw4_chunks_overflow", 16, 250, 520, 12, False, True, (4, 1, 4)),
