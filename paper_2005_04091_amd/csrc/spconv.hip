@@ -208,6 +208,84 @@ __global__ __launch_bounds__(kThreads) void resize_pad_rows_kernel(ResizeArgs a,
     }
 }
 
+// Plane variant, for small planes (source and padded output): a workgroup
+// copies ppw consecutive source planes into LDS with coalesced loads (16
+// bytes per lane when aligned), then writes their padded output planes as one
+// flat range, each wave round one coalesced streaming store, reading each
+// element's four taps from LDS. Tap tables and interpolation order are the
+// flat variant's, so both give the same bits. Replaces that variant's four
+// gathers from global memory per element by one streamed read of the source.
+constexpr int kResizePlaneMaxIn = 4096;       // source floats per plane
+constexpr int kResizePlaneMaxOut = 16384;     // padded output floats per plane
+constexpr int kResizePlaneLds = 48 * 1024;    // bytes of staged source per workgroup
+constexpr long long kResizePlaneWgs = 1024;   // planes per workgroup grow while the grid keeps this many
+
+struct ResizePlaneArgs {
+    int Hin, Win, H, W, pad, Hp, Wp;
+    int ps;               // Hp * Wp
+    int in_ps;            // Hin * Win
+    int ppw;              // planes per workgroup
+    int vec;              // 16-byte source loads (aligned tensor, in_ps % 4 == 0)
+    long long planes;
+    uint32_t ps_magic, wp_magic;  // x / ps, x / Wp as multiply-shift
+    int ps_shift, wp_shift;
+};
+
+__global__ __launch_bounds__(kThreads) void resize_pad_plane_kernel(ResizePlaneArgs a, const float *__restrict__ in,
+                                                                    float *__restrict__ out) {
+    extern __shared__ int tab[];
+    const int nt = a.Hp + a.Wp;
+    int *tap0 = tab;
+    int *tap1 = tab + nt;
+    float *tapw = reinterpret_cast<float *>(tab + 2 * nt);
+    float *src = reinterpret_cast<float *>(tab + ((3 * nt + 3) & ~3));
+    for (int i = (int)threadIdx.x; i < nt; i += kThreads) {
+        const bool row = i < a.Hp;
+        const int o = (row ? i : i - a.Hp) - a.pad;
+        const int n_out = row ? a.H : a.W;
+        const int scale = row ? a.Win : 1;
+        int t0 = -1, t1 = 0;
+        float w = 0.0f;
+        if (o >= 0 && o < n_out) {
+            const ResizeTap r = resize_tap(o, row ? a.Hin : a.Win, n_out);
+            t0 = r.i0 * scale;
+            t1 = r.i1 * scale;
+            w = r.t;
+        }
+        tap0[i] = t0;
+        tap1[i] = t1;
+        tapw[i] = w;
+    }
+    const long long p0 = (long long)blockIdx.x * a.ppw;
+    const int np = (int)min((long long)a.ppw, a.planes - p0);
+    const float *sp = in + p0 * a.in_ps;
+    const int n = np * a.in_ps;
+    if (a.vec) {
+        for (int i = (int)threadIdx.x * 4; i < n; i += kThreads * 4)
+            *reinterpret_cast<float4 *>(src + i) = *reinterpret_cast<const float4 *>(sp + i);
+    } else {
+        for (int i = (int)threadIdx.x; i < n; i += kThreads) src[i] = sp[i];
+    }
+    __syncthreads();
+    float *op = out + p0 * a.ps;
+    const int m = np * a.ps;
+    for (int e = (int)threadIdx.x; e < m; e += kThreads) {
+        const int q = (int)fast_div((uint32_t)e, a.ps_magic, a.ps_shift);
+        const int ee = e - q * a.ps;
+        const int yp = (int)fast_div((uint32_t)ee, a.wp_magic, a.wp_shift);
+        const int xp = ee - yp * a.Wp;
+        const int r0 = tap0[yp], c0 = tap0[a.Hp + xp];
+        float o = 0.0f;
+        if ((r0 | c0) >= 0) {
+            const int r1 = tap1[yp], c1 = tap1[a.Hp + xp];
+            const float tx = tapw[a.Hp + xp];
+            const float *pl = src + q * a.in_ps;
+            o = lerp_f(lerp_f(pl[r0 + c0], pl[r0 + c1], tx), lerp_f(pl[r1 + c0], pl[r1 + c1], tx), tapw[yp]);
+        }
+        stream_store(op + e, o);
+    }
+}
+
 // Flat variant for planes whose two tap tables fit in LDS (Hp + Wp entries):
 // the padded output of all planes is one flat array, each thread takes
 // kResizeFlatElems elements 256 apart (every lane busy whatever the width, each
@@ -1524,9 +1602,37 @@ extern "C" int spconv_resize_pad_input(const float *in, int N, int C, int Hin, i
     const long long planes = (long long)N * C;
     if (Hp * Wp >= (1LL << 31) || planes * Hp * Wp >= (1LL << 40) || planes * Hin * Win >= (1LL << 40))
         return SPCONV_EINVAL;
+    const long long ps = Hp * Wp;
+    const long long in_ps = (long long)Hin * Win;
+    // Plane kernel when a source plane and its padded output are small (tap
+    // tables of at most 12 KiB plus at most 48 KiB of staged planes).
+    if (in_ps <= kResizePlaneMaxIn && ps <= kResizePlaneMaxOut && Hp + Wp <= 1024) {
+        ResizePlaneArgs g;
+        g.Hin = Hin;
+        g.Win = Win;
+        g.H = H;
+        g.W = W;
+        g.pad = pad;
+        g.Hp = (int)Hp;
+        g.Wp = (int)Wp;
+        g.ps = (int)ps;
+        g.in_ps = (int)in_ps;
+        g.planes = planes;
+        const long long by_lds = std::max(1LL, (long long)kResizePlaneLds / (in_ps * (long long)sizeof(float)));
+        const long long by_grid = std::max(1LL, planes / kResizePlaneWgs);
+        g.ppw = (int)std::min(by_lds, by_grid);
+        g.vec = (in_ps % 4 == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0) ? 1 : 0;
+        if (!div_magic((uint32_t)ps, &g.ps_magic, &g.ps_shift) || !div_magic((uint32_t)Wp, &g.wp_magic, &g.wp_shift))
+            return SPCONV_EINVAL;
+        const long long blocks = (planes + g.ppw - 1) / g.ppw;
+        if (blocks > 0x7fffffffLL) return SPCONV_EINVAL;
+        const size_t lds = (size_t)((3 * (Hp + Wp) + 3) & ~3LL) * sizeof(int) + (size_t)g.ppw * in_ps * sizeof(float);
+        hipLaunchKernelGGL(resize_pad_plane_kernel, dim3((unsigned)blocks), dim3(kThreads), lds, stream, g, in,
+                           out_padded);
+        return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
+    }
     // Flat kernel when both tap tables fit in LDS and the source planes one
     // workgroup can touch are addressable with 32-bit offsets (in elements).
-    const long long ps = Hp * Wp;
     const long long span_planes = (long long)kThreads * kResizeFlatElems / ps + 2;
     if (Hp + Wp <= kResizeFlatMaxTab && span_planes * Hin * Win < (1LL << 31)) {
         ResizeFlatArgs f;
