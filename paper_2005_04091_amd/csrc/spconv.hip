@@ -218,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void resize_pad_rows_kernel(ResizeArgs a,
 constexpr int kResizePlaneMaxIn = 4096;       // source floats per plane
 constexpr int kResizePlaneMaxOut = 16384;     // padded output floats per plane
 constexpr int kResizePlaneLds = 48 * 1024;    // bytes of staged source per workgroup
-constexpr long long kResizePlaneWgs = 1024;   // planes per workgroup grow while the grid keeps this many
+constexpr long long kResizePlaneWgs = 2048;   // planes per workgroup grow while the grid keeps this many
 
 struct ResizePlaneArgs {
     int Hin, Win, H, W, pad, Hp, Wp;
