@@ -65,9 +65,6 @@ typedef struct spconv_csr {
     const int32_t *colidx; /* [nnz]; not read by spconv_forward (may be NULL there) */
     const int32_t *offset; /* [nnz] */
     const float *vals;     /* [nnz]; the filter values, bit-copied */
-    int64_t max_row_nnz;   /* optional planning hint for spconv_forward: the largest row's entry
-                              count (rowptr[k+1] - rowptr[k]), or 0 if unknown. It only steers the
-                              choice of tiling; results do not depend on it. Must lie in [0, nnz]. */
 } spconv_csr;
 
 /*
@@ -160,7 +157,7 @@ int spconv_resize_pad_input(const float *in, int N, int C, int Hin, int Win, int
  * Summation order inside one output is unspecified (fp32 arithmetic; results
  * are reproducible run to run for a given device and shape).
  * Errors: SPCONV_EINVAL (NULL pointer, sizes < 1, stride < 1, pad < 0, shape
- * mismatch with csr, nnz outside [0, 2^31), csr->max_row_nnz outside [0, nnz],
+ * mismatch with csr, nnz outside [0, 2^31),
  * unknown flag bits, SPCONV_UNPADDED_INPUT with a plan other than the
  * stride-1 kernel, empty output,
  * Ho or Wo < 2 with the pool flag, C*Hp*Wp >= 2^31); SPCONV_EHIP when the
@@ -170,8 +167,9 @@ int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spc
                    int stride, int pad, const float *bias, uint32_t flags, float *out, hipStream_t stream);
 
 /*
- * Epilogue options of spconv_forward_ex: where the fused output goes and what is
- * added before the activation. A zero-initialised struct gives spconv_forward's
+ * Options of spconv_forward_ex (and of spconv_plan / spconv_forward_dense):
+ * where the fused output goes, what is added before the activation, and a
+ * planning hint. A zero-initialised struct (or NULL) gives spconv_forward's
  * behaviour.
  *
  * out_pad   >= 0. The stored output planes carry a border of out_pad zeros:
@@ -190,30 +188,40 @@ int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spc
  *           "Evaluation"), read straight from a padded block input when
  *           residual_pad equals that input's pad. Must not overlap out.
  * residual_pad >= 0, ignored without a residual.
+ * max_row_nnz  planning hint, 0 = unknown: the largest CSR row's entry count
+ *           (rowptr[k+1] - rowptr[k] over k). The CSR arrays live in device
+ *           memory and the planner never reads them back (that would need a
+ *           synchronous copy inside an asynchronous call), so this is how it
+ *           learns that a filter's rows are skewed, where pairing heavy and
+ *           light output channels on one wave pays. It only steers the choice
+ *           of tiling: results do not depend on it. Must lie in [0, nnz]
+ *           (spconv_forward_dense ignores it).
  * Both borders are limited so that one padded plane has fewer than 2^31
  * elements.
  */
-typedef struct spconv_epilogue {
+typedef struct spconv_options {
     int32_t out_pad;
     int32_t residual_pad;
     const float *residual;
-} spconv_epilogue;
+    int64_t max_row_nnz;
+} spconv_options;
 
 /*
- * spconv_forward_ex - spconv_forward with epilogue options (device, asynchronous,
- * one kernel, one store per output element including the border).
+ * spconv_forward_ex - spconv_forward with options (device, asynchronous, one
+ * kernel, one store per output element including the border).
  *
  *   pre = bias[k] + sum_j vals[j] * in_padded[...]      (as spconv_forward)
- *         + residual[n,k,y,x]                           (epi->residual != NULL)
+ *         + residual[n,k,y,x]                           (opt->residual != NULL)
  *   o   = RELU ? max(pre, 0) : pre;   q = MAXPOOL2X2 ? 2x2 max of o : o
  *   out[n][k][i+out_pad][j+out_pad] = q[n,k,i,j];  border of out = +0.0
  *
- * epi: host struct, nullable (= all zero). Other arguments, layouts and errors
+ * opt: host struct, nullable (= all zero). Other arguments, layouts and errors
  * as spconv_forward; additionally SPCONV_EINVAL for a negative out_pad or
- * residual_pad, or a padded output or residual plane of 2^31 elements or more.
+ * residual_pad, a padded output or residual plane of 2^31 elements or more, or
+ * max_row_nnz outside [0, nnz].
  */
 int spconv_forward_ex(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S,
-                      int stride, int pad, const float *bias, uint32_t flags, const spconv_epilogue *epi, float *out,
+                      int stride, int pad, const float *bias, uint32_t flags, const spconv_options *opt, float *out,
                       hipStream_t stream);
 
 /* Kernel families reported by spconv_plan. */
@@ -236,16 +244,32 @@ typedef struct spconv_plan_info {
 } spconv_plan_info;
 
 /*
- * spconv_plan - the launch plan spconv_forward would use for these arguments
- * (host only, queues nothing). Takes the same arguments as spconv_forward
- * without the buffers and applies the same checks; csr's arrays are not read.
- * Meant for tests, tools and reports that need to know which kernel variant
- * and tiling run.
- * Errors: those of spconv_forward's argument checks; SPCONV_EINVAL for a NULL
- * info.
+ * spconv_plan - the launch plan spconv_forward_ex would use for these arguments
+ * (host only, queues nothing). Takes the same arguments as spconv_forward_ex
+ * without the buffers and applies the same checks (opt nullable; only its
+ * max_row_nnz steers the plan); csr's arrays are not read. Meant for tests,
+ * tools and reports that need to know which kernel variant and tiling run.
+ * Errors: those of spconv_forward_ex's argument checks; SPCONV_EINVAL for a
+ * NULL info.
  */
 int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride, int pad,
-                uint32_t flags, spconv_plan_info *info);
+                uint32_t flags, const spconv_options *opt, spconv_plan_info *info);
+
+/*
+ * spconv_kernel_variants - the compiled instances of one kernel family (host
+ * only), for tests and reports that must show every instance the planners can
+ * pick has been run. Each instance is a 4-tuple of int32:
+ *   SPCONV_KERNEL_STRIDE1  (pixels_per_lane, images_per_group, channels_per_wave, pool)
+ *   SPCONV_KERNEL_GENERIC  (pixels_per_lane, 0, channels_per_workgroup, pool)
+ *   SPCONV_KERNEL_DENSE    (R, S, pixel blocks per wave, pool)
+ * with pool 0 or 1 and the other fields as spconv_plan_info reports them.
+ * variants  host array of 4*capacity int32, nullable when capacity is 0; the
+ *           first min(count, capacity) tuples are written.
+ * count     host, required: receives the number of instances.
+ * Errors: SPCONV_EINVAL for an unknown family, a NULL count, a negative
+ * capacity, or a NULL variants with capacity > 0.
+ */
+int spconv_kernel_variants(int32_t kernel, int32_t *variants, int32_t capacity, int32_t *count);
 
 /*
  * Dense path. Above some density, skipping zeros no longer pays: the same
@@ -284,20 +308,20 @@ int spconv_pack_dense(const float *w, const uint8_t *mask, int K, int C, int R, 
 /*
  * spconv_forward_dense - spconv_forward_ex computed from the packed dense
  * filter (device, asynchronous): same padded (or, with SPCONV_UNPADDED_INPUT,
- * unpadded) input, bias, flags, epilogue
- * options, output layout and ordering; the result is the same convolution up
+ * unpadded) input, bias, flags, options (max_row_nnz ignored), output layout
+ * and ordering; the result is the same convolution up
  * to fp32 summation order. Stride 1 only (the stride is not an argument);
  * filters 3x3 and 1x1.
  * packed  device copy of spconv_pack_dense's output for this K, C, R, S.
  * Errors: SPCONV_EINVAL (NULL in_padded/packed/out, sizes < 1, pad < 0, a
  * filter other than 3x3 or 1x1, unknown flags, pool with Ho or Wo < 2,
- * C*Hp*Wp >= 2^31, a packed filter of 2^31 bytes or more, bad epilogue
+ * C*Hp*Wp >= 2^31, a packed filter of 2^31 bytes or more, bad border
  * options as in spconv_forward_ex, or no tiling
  * that fits the kernel: the padded row wider than 255 floats, 127 with pool);
  * SPCONV_EHIP when the launch fails.
  */
 int spconv_forward_dense(const float *in_padded, int N, int C, int H, int W, const float *packed, int K, int R, int S,
-                         int pad, const float *bias, uint32_t flags, const spconv_epilogue *epi, float *out,
+                         int pad, const float *bias, uint32_t flags, const spconv_options *opt, float *out,
                          hipStream_t stream);
 
 /*
@@ -322,14 +346,25 @@ int spconv_select_path(int N, int C, int H, int W, int K, int R, int S, int stri
                        uint32_t flags, int *path);
 
 /*
- * spconv_output_shape - stored output plane size for the given layer.
+ * spconv_output_shape - stored output plane size for the given layer (host).
+ * The convolution's output grid is that of the paper's dense convolution
+ * written in its DSL section (an output pixel for every position where the
+ * R x S filter fits), taken over the zero-padded input:
+ *   Ho = (H + 2*pad - R)/stride + 1,  Wo = (W + 2*pad - S)/stride + 1  (floor);
+ * with SPCONV_MAXPOOL2X2 the 2x2, stride-2 max-pool of the Conv-Relu-Maxpool
+ * block (Evaluation) halves both, dropping an odd last row/column.
  * Writes *Ho, *Wo (pooled sizes when flags has SPCONV_MAXPOOL2X2).
  * Errors: SPCONV_EINVAL for NULL outputs, H/W/R/S/stride < 1, pad < 0, unknown
  * flags, or an empty (pooled) output.
  */
 int spconv_output_shape(int H, int W, int R, int S, int stride, int pad, uint32_t flags, int *Ho, int *Wo);
 
-/* spconv_strerror - static, human-readable text for a status code. */
+/*
+ * spconv_strerror - static, human-readable text for one of this library's
+ * status codes (SPCONV_OK, SPCONV_EINVAL, SPCONV_ECAPACITY, SPCONV_EHIP; any
+ * other value gives a generic text). Not an operation of the paper: the
+ * status codes are this C ABI's own. Never NULL; the text must not be freed.
+ */
 const char *spconv_strerror(int code);
 
 #ifdef __cplusplus

@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
+#include <set>
+#include <utility>
 
 namespace {
 
@@ -71,6 +74,24 @@ inline bool div_magic(uint32_t d, uint32_t *magic, int *shift) {
     if (m > 0xffffffffull) return false;
     *magic = (uint32_t)m;
     *shift = s;
+    return true;
+}
+
+// Raise a kernel instance's dynamic-LDS limit to `bytes` on the current
+// device, once per (device, instance). Every caller of one instance passes
+// the same value (the most any plan of its family uses), so launches of
+// different shapes from several host threads never lower the limit under
+// one another.
+inline bool raise_lds_limit(const void *fn, int bytes) {
+    static std::mutex mu;
+    static std::set<std::pair<int, const void *>> done;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    std::lock_guard<std::mutex> lock(mu);
+    if (done.count({dev, fn})) return true;
+    if (bytes > 65536 && hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) != hipSuccess)
+        return false;
+    done.insert({dev, fn});
     return true;
 }
 

@@ -28,14 +28,16 @@
 #include <cstdint>
 
 #include "common.h"
+#include "dense_layout.h"
 #include "spconv.h"
+
+__attribute__((visibility("hidden"))) int dense_kernel_variants(int32_t *variants, int32_t capacity, int32_t *count);
 
 namespace {
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kDnsTile = 32;              // MFMA tile: 32 channels x 32 pixels
-constexpr int kDnsMaxWaves = 4;           // channel tiles (of 32) per workgroup
+constexpr int kDnsTile = dense_layout::kTile;  // MFMA tile: 32 channels x 32 pixels
 constexpr int kDnsMaxThreads = 512;       // nw * ks waves per workgroup, at most 8
 constexpr int kDnsMaxBlocks = 8;          // pixel blocks per wave (16 accumulator VGPRs each)
 constexpr int kDnsBlock = 256;            // floats per 16-byte-per-lane LDS DMA instruction
@@ -408,17 +410,41 @@ DenseKernel pick_dense(int R, int S, int NB, bool pool) {
     return nullptr;
 }
 
+}  // namespace
+
+// (R, S, blocks per wave, pool) of every compiled dense instance (a library-
+// internal helper of spconv_kernel_variants, not exported).
+__attribute__((visibility("hidden"))) int dense_kernel_variants(int32_t *variants, int32_t capacity, int32_t *count) {
+    int n = 0;
+    for (int rs : {3, 1})
+        for (int nb = 1; nb <= kDnsMaxBlocks; ++nb)
+            for (int pool = 0; pool < 2; ++pool)
+                if (pick_dense(rs, rs, nb, pool != 0)) {
+                    if (n < capacity) {
+                        variants[4 * n] = rs;
+                        variants[4 * n + 1] = rs;
+                        variants[4 * n + 2] = nb;
+                        variants[4 * n + 3] = pool;
+                    }
+                    ++n;
+                }
+    *count = n;
+    return SPCONV_OK;
+}
+
+namespace {
+
 struct DensePlan {
     int TH = 0, ntiles_y = 0, NB = 0, nw = 0, ks = 1, nkt = 0, Cc = 0, nchunks = 0, PLp = 0, total_wgs = 0;
     size_t lds_bytes = 0;
 };
 
-int round_up(int a, int b) { return (a + b - 1) / b * b; }
+using dense_layout::round_up;
 
-int dense_waves(int K) { return std::min(kDnsMaxWaves, (K + kDnsTile - 1) / kDnsTile); }
+int dense_waves(int K) { return dense_layout::waves(K); }
 
 // Kp of the packed filter: K rounded up to whole workgroup channel tiles.
-int dense_kp(int K) { return round_up(K, kDnsTile * dense_waves(K)); }
+int dense_kp(int K) { return dense_layout::kp(K); }
 
 // Waves that split the reduction over channel pairs (1, 2 or 4), each adding
 // a 32-channel partial tile that is summed through LDS: 2 where the workgroup
@@ -491,6 +517,7 @@ bool plan_dense(int N, int C, int K, int Wp, int Ho, int R, int S, bool pool, De
     size_t lds = (size_t)2 * p.Cc * p.PLp * sizeof(float);
     if (pool) lds = std::max(lds, (size_t)p.nw * kDnsPoolCh * p.NB * kDnsTile * sizeof(float));
     if (p.ks > 1) lds = std::max(lds, (size_t)p.nw * p.NB * 16 * kWave * sizeof(float));
+    if (lds > (size_t)kDnsLdsBytes) return false;
     p.lds_bytes = lds;
     const long long wgs = (long long)N * p.ntiles_y * p.nkt;
     if (wgs > 0x7fffffffLL) return false;
@@ -508,7 +535,7 @@ bool out_extent(int in, int k, int pad, int *o) {
 
 // Checks and plan of a dense forward call (everything but the buffers).
 int prepare_dense(int N, int C, int H, int W, int K, int R, int S, int pad, uint32_t flags,
-                  const spconv_epilogue *epi, DensePlan *plp, DenseArgs *ap) {
+                  const spconv_options *opt, DensePlan *plp, DenseArgs *ap) {
     if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || pad < 0) return SPCONV_EINVAL;
     if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2 | SPCONV_UNPADDED_INPUT)) return SPCONV_EINVAL;
     const long long Hp = (long long)H + 2LL * pad, Wp = (long long)W + 2LL * pad;
@@ -557,8 +584,8 @@ int prepare_dense(int N, int C, int H, int W, int K, int R, int S, int pad, uint
     a.buf_floats = pl.Cc * pl.PLp;
     a.total_floats = (size_t)N * C * Hp * Wp;
     a.total_wgs = pl.total_wgs;
-    const long long op = epi ? epi->out_pad : 0;
-    const long long rp = (epi && epi->residual) ? epi->residual_pad : 0;
+    const long long op = opt ? opt->out_pad : 0;
+    const long long rp = (opt && opt->residual) ? opt->residual_pad : 0;
     if (op < 0 || rp < 0) return SPCONV_EINVAL;
     const long long oh = a.Hq + 2 * op, ow = a.Wq + 2 * op;
     const long long rh = a.Ho + 2 * rp, rw = a.Wo + 2 * rp;
@@ -576,28 +603,18 @@ int prepare_dense(int N, int C, int H, int W, int K, int R, int S, int pad, uint
 
 }  // namespace
 
-extern "C" int spconv_dense_size(int K, int C, int R, int S, int64_t *floats) {
-    if (!floats || K < 1 || C < 1 || R < 1 || S < 1) return SPCONV_EINVAL;
-    const long long v = (long long)((C + 1) / 2) * R * S * dense_kp(K) * 2;
-    if (v >= (1LL << 40)) return SPCONV_EINVAL;
-    *floats = v;
-    return SPCONV_OK;
-}
-
 extern "C" int spconv_forward_dense(const float *in_padded, int N, int C, int H, int W, const float *packed, int K,
                                     int R, int S, int pad, const float *bias, uint32_t flags,
-                                    const spconv_epilogue *epi, float *out, hipStream_t stream) {
+                                    const spconv_options *opt, float *out, hipStream_t stream) {
     if (!in_padded || !packed || !out) return SPCONV_EINVAL;
     DensePlan pl;
     DenseArgs a;
-    const int rc = prepare_dense(N, C, H, W, K, R, S, pad, flags, epi, &pl, &a);
+    const int rc = prepare_dense(N, C, H, W, K, R, S, pad, flags, opt, &pl, &a);
     if (rc != SPCONV_OK) return rc;
     DenseKernel kern = pick_dense(R, S, pl.NB, (flags & SPCONV_MAXPOOL2X2) != 0);
-    const float *residual = epi ? epi->residual : nullptr;
-    if (pl.lds_bytes > 65536 &&
-        hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds_bytes) !=
-            hipSuccess)
-        return SPCONV_EHIP;
+    const float *residual = opt ? opt->residual : nullptr;
+    // Raised once per instance to the family's budget (see raise_lds_limit).
+    if (!raise_lds_limit((const void *)kern, kDnsLdsBytes)) return SPCONV_EHIP;
     hipLaunchKernelGGL(kern, dim3((unsigned)pl.total_wgs), dim3((unsigned)(pl.nw * pl.ks * kWave)), pl.lds_bytes, stream, a,
                        in_padded, packed, bias, residual, out);
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;

@@ -9,6 +9,7 @@
 #include <cstring>
 #include <limits>
 
+#include "dense_layout.h"
 #include "spconv.h"
 
 namespace {
@@ -67,6 +68,14 @@ extern "C" int spconv_pack_csr(const float *w, const uint8_t *mask, int K, int C
             }
         }
     }
+    return SPCONV_OK;
+}
+
+extern "C" int spconv_dense_size(int K, int C, int R, int S, int64_t *floats) {
+    if (!floats || K < 1 || C < 1 || R < 1 || S < 1) return SPCONV_EINVAL;
+    const long long v = (long long)((C + 1) / 2) * R * S * dense_layout::kp(K) * 2;
+    if (v >= (1LL << 40)) return SPCONV_EINVAL;
+    *floats = v;
     return SPCONV_OK;
 }
 

@@ -40,11 +40,15 @@
 #include "common.h"
 #include "spconv.h"
 
+// Instances of the dense kernel (dense.hip), for spconv_kernel_variants.
+__attribute__((visibility("hidden"))) int dense_kernel_variants(int32_t *variants, int32_t capacity, int32_t *count);
+
 namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWave * kWaves;
 constexpr int kLdsBudgetFloats = 20480;   // generic kernel: 80 KiB of LDS per workgroup (two per CU)
+constexpr int kGenericLdsBytes = kLdsBudgetFloats * 4;
 
 
 // ---------------------------------------------------------------------------
@@ -1311,41 +1315,59 @@ struct Plan {
 using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_t *, const float *, const float *,
                           const float *, float *);
 
-template <int PI, int IPW>
-FwdKernel pick_s1_rpw(int RPW, bool pool) {
-    // Four waves per SIMD leave 128 VGPRs per lane: two accumulator sets of
-    // RPW * IPW * PI (even and odd taps) plus two pipeline buffers of IPW * PI,
-    // kept at or below 96, the largest tilings that compile without spills.
-    if constexpr (PI * IPW <= 8)
-        if (RPW == 4) return pool ? spconv_s1_kernel<PI, IPW, 4, true> : spconv_s1_kernel<PI, IPW, 4, false>;
-    if constexpr (PI * IPW <= 16)
-        if (RPW == 2) return pool ? spconv_s1_kernel<PI, IPW, 2, true> : spconv_s1_kernel<PI, IPW, 2, false>;
-    if constexpr (PI * IPW <= 24)
-        if (RPW == 1) return pool ? spconv_s1_kernel<PI, IPW, 1, true> : spconv_s1_kernel<PI, IPW, 1, false>;
-    return nullptr;
+// Stride-1 kernel instances: (PI, IPW, RPW, pools), pools bit 0 = built
+// without the pool epilogue, bit 1 = with it. Four waves per SIMD leave 128
+// VGPRs per lane: two accumulator sets of RPW * IPW * PI floats (even and odd
+// taps) plus the pipeline buffers, so IPW * PI <= 24 and RPW * IPW * PI <= 32
+// (at most 16 pixels with two channels, 8 with four). The list holds the
+// instances the planner can pick; the GPU tests run each one against the
+// oracle.
+struct S1Variant {
+    int pi, ipw, rpw, pools;
+};
+constexpr S1Variant kS1Variants[] = {
+    // one image per tile
+    {24, 1, 1, 3}, {22, 1, 1, 3}, {20, 1, 1, 3}, {18, 1, 1, 3}, {16, 1, 1, 3}, {14, 1, 1, 3}, {12, 1, 1, 3},
+    {10, 1, 1, 3}, {8, 1, 1, 3},  {6, 1, 1, 3},  {4, 1, 1, 3},
+    {16, 1, 2, 3}, {14, 1, 2, 3}, {12, 1, 2, 3}, {10, 1, 2, 3}, {8, 1, 2, 3}, {6, 1, 2, 3}, {4, 1, 2, 3},
+    {8, 1, 4, 3},  {6, 1, 4, 3},  {4, 1, 4, 3},
+    // two images per tile
+    {8, 2, 1, 3}, {6, 2, 1, 3}, {4, 2, 1, 3}, {2, 2, 1, 3},
+    {8, 2, 2, 3}, {6, 2, 2, 3}, {4, 2, 2, 3}, {2, 2, 2, 3},
+    {4, 2, 4, 3}, {2, 2, 4, 3},
+    // four images per tile
+    {6, 4, 1, 3}, {4, 4, 1, 3}, {2, 4, 1, 3},
+    {4, 4, 2, 3}, {2, 4, 2, 3},
+    {2, 4, 4, 3},
+};
+constexpr int kNumS1Variants = (int)(sizeof(kS1Variants) / sizeof(kS1Variants[0]));
+
+template <int I>
+FwdKernel pick_s1_from(int PI, int IPW, int RPW, bool pool) {
+    if constexpr (I == kNumS1Variants) {
+        return nullptr;
+    } else {
+        constexpr S1Variant v = kS1Variants[I];
+        static_assert(v.ipw * v.pi <= 24 && v.rpw * v.ipw * v.pi <= 32 && v.pi % 2 == 0,
+                      "tiling exceeds the register budget");
+        if (v.pi == PI && v.ipw == IPW && v.rpw == RPW) {
+            if (pool) {
+                if constexpr ((v.pools & 2) != 0) return spconv_s1_kernel<v.pi, v.ipw, v.rpw, true>;
+                return nullptr;
+            }
+            if constexpr ((v.pools & 1) != 0) return spconv_s1_kernel<v.pi, v.ipw, v.rpw, false>;
+            return nullptr;
+        }
+        return pick_s1_from<I + 1>(PI, IPW, RPW, pool);
+    }
 }
 
-template <int IPW, int... PIs>
-FwdKernel pick_s1_pi(int PI, int RPW, bool pool) {
-    FwdKernel k = nullptr;
-    ((PI == PIs ? (k = pick_s1_rpw<PIs, IPW>(RPW, pool), 0) : 0), ...);
-    return k;
-}
-
-// Pixels per lane per image (PI), images per wave (IPW) and channels per wave
-// (RPW) the stride-1 kernel is built for.
+// Pixels per lane per image (PI) the planner tries with one image per tile
+// and with several.
 constexpr int kPiSingle[] = {24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4};
 constexpr int kPiMulti[] = {8, 6, 4, 2};
 
-FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool) {
-    switch (IPW) {
-        case 1:
-            return pick_s1_pi<1, 24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4>(PI, RPW, pool);
-        case 2: return pick_s1_pi<2, 8, 6, 4, 2>(PI, RPW, pool);
-        case 4: return pick_s1_pi<4, 8, 6, 4, 2>(PI, RPW, pool);
-        default: return nullptr;
-    }
-}
+FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool) { return pick_s1_from<0>(PI, IPW, RPW, pool); }
 
 // Picks the stride-1 tiling with the smallest modelled run time. The model
 // counts LDS cycles: every nonzero costs a wave IPW*PI LDS reads (2 cycles
@@ -1680,7 +1702,7 @@ namespace {
 // Host-side checks of a forward call (everything but the buffer pointers) and
 // its launch plan. Returns SPCONV_OK or SPCONV_EINVAL.
 int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride, int pad,
-                    uint32_t flags, Plan *plp, FwdArgs *ap) {
+                    uint32_t flags, long long max_row_nnz, Plan *plp, FwdArgs *ap) {
     if (!csr) return SPCONV_EINVAL;
     if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 || pad < 0) return SPCONV_EINVAL;
     if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2 | SPCONV_UNPADDED_INPUT)) return SPCONV_EINVAL;
@@ -1688,7 +1710,7 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     const long long Hp = (long long)H + 2LL * pad, Wp = (long long)W + 2LL * pad;
     if (csr->Hp != Hp || csr->Wp != Wp) return SPCONV_EINVAL;
     if (csr->nnz < 0 || csr->nnz >= (1LL << 31)) return SPCONV_EINVAL;
-    if (csr->max_row_nnz < 0 || csr->max_row_nnz > csr->nnz) return SPCONV_EINVAL;
+    if (max_row_nnz < 0 || max_row_nnz > csr->nnz) return SPCONV_EINVAL;
     if (!csr->rowptr || (csr->nnz > 0 && (!csr->offset || !csr->vals))) return SPCONV_EINVAL;
     if ((long long)C * Hp * Wp >= (1LL << 31)) return SPCONV_EINVAL;
     const bool pool = (flags & SPCONV_MAXPOOL2X2) != 0;
@@ -1710,11 +1732,10 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     } else {
         if (row16)
             ok = plan_stride1(N, C, K, (int)Hp, (int)Wp, ((int)Wp + 3) / 4 * 4, (4 - pad % 4) % 4, Ho, Wo, R, S,
-                              pool, csr->nnz, csr->max_row_nnz, &pl);
+                              pool, csr->nnz, max_row_nnz, &pl);
         if (!ok) {
             row16 = false;
-            ok = plan_stride1(N, C, K, (int)Hp, (int)Wp, (int)Wp, 0, Ho, Wo, R, S, pool, csr->nnz, csr->max_row_nnz,
-                              &pl);
+            ok = plan_stride1(N, C, K, (int)Hp, (int)Wp, (int)Wp, 0, Ho, Wo, R, S, pool, csr->nnz, max_row_nnz, &pl);
         }
     }
     if (!ok) return SPCONV_EINVAL;
@@ -1779,11 +1800,12 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     return SPCONV_OK;
 }
 
-// Epilogue options of spconv_forward_ex, checked and folded into the args.
-int apply_epilogue(const spconv_epilogue *epi, FwdArgs *a) {
-    if (!epi) return SPCONV_OK;
-    if (epi->out_pad < 0 || (epi->residual && epi->residual_pad < 0)) return SPCONV_EINVAL;
-    const long long op = epi->out_pad, rp = epi->residual ? epi->residual_pad : 0;
+// Border and residual options of spconv_forward_ex, checked and folded into
+// the args.
+int apply_epilogue(const spconv_options *opt, FwdArgs *a) {
+    if (!opt) return SPCONV_OK;
+    if (opt->out_pad < 0 || (opt->residual && opt->residual_pad < 0)) return SPCONV_EINVAL;
+    const long long op = opt->out_pad, rp = opt->residual ? opt->residual_pad : 0;
     const long long oh = a->Hq + 2 * op, ow = a->Wq + 2 * op;
     const long long rh = a->Ho + 2 * rp, rw = a->Wo + 2 * rp;
     if (oh * ow >= (1LL << 31) || rh * rw >= (1LL << 31)) return SPCONV_EINVAL;
@@ -1800,15 +1822,15 @@ int apply_epilogue(const spconv_epilogue *epi, FwdArgs *a) {
 
 extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, int W, const spconv_csr *csr, int K,
                                  int R, int S, int stride, int pad, const float *bias, uint32_t flags,
-                                 const spconv_epilogue *epi, float *out, hipStream_t stream) {
+                                 const spconv_options *opt, float *out, hipStream_t stream) {
     if (!in_padded || !out) return SPCONV_EINVAL;
     Plan pl;
     FwdArgs a;
-    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, &pl, &a);
+    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, &pl, &a);
     if (rc != SPCONV_OK) return rc;
-    rc = apply_epilogue(epi, &a);
+    rc = apply_epilogue(opt, &a);
     if (rc != SPCONV_OK) return rc;
-    const float *residual = epi ? epi->residual : nullptr;
+    const float *residual = opt ? opt->residual : nullptr;
     // 16-byte row copies need a 16-byte aligned tensor; otherwise the same
     // layout is filled 4 bytes per lane.
     if (a.dma16 && (reinterpret_cast<uintptr_t>(in_padded) & 15) != 0) a.dma16 = 0;
@@ -1820,9 +1842,10 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
                    (!residual || (reinterpret_cast<uintptr_t>(residual) & 3) == 0);
     FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0);
     const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
-    if (pl.lds_bytes > 65536 &&
-        hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds_bytes) !=
-            hipSuccess)
+    // Each kernel instance's dynamic-LDS limit is raised once, to the most any
+    // plan of its family uses, so that launches of different shapes from
+    // several host threads never lower it under one another.
+    if (!raise_lds_limit((const void *)kern, pl.kind == Kind::kStride1 ? kS1LdsFloats * 4 : kGenericLdsBytes))
         return SPCONV_EHIP;
     hipLaunchKernelGGL(kern, dim3((unsigned)pl.total_wgs), dim3(threads), pl.lds_bytes, stream, a, in_padded,
                        csr->rowptr, csr->offset, csr->vals, bias, residual, out);
@@ -1836,11 +1859,13 @@ extern "C" int spconv_forward(const float *in_padded, int N, int C, int H, int W
 }
 
 extern "C" int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride,
-                           int pad, uint32_t flags, spconv_plan_info *info) {
+                           int pad, uint32_t flags, const spconv_options *opt, spconv_plan_info *info) {
     if (!info) return SPCONV_EINVAL;
     Plan pl;
     FwdArgs a;
-    const int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, &pl, &a);
+    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, &pl, &a);
+    if (rc != SPCONV_OK) return rc;
+    rc = apply_epilogue(opt, &a);
     if (rc != SPCONV_OK) return rc;
     const bool s1 = pl.kind == Kind::kStride1;
     info->kernel = s1 ? SPCONV_KERNEL_STRIDE1 : SPCONV_KERNEL_GENERIC;
@@ -1854,5 +1879,31 @@ extern "C" int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, in
     info->workgroups = pl.total_wgs;
     info->threads_per_workgroup = (int32_t)(s1 ? kS1Threads : kThreads);
     info->lds_bytes = (int64_t)pl.lds_bytes;
+    return SPCONV_OK;
+}
+
+extern "C" int spconv_kernel_variants(int32_t kernel, int32_t *variants, int32_t capacity, int32_t *count) {
+    if (!count || capacity < 0 || (capacity > 0 && !variants)) return SPCONV_EINVAL;
+    if (kernel == SPCONV_KERNEL_DENSE) return dense_kernel_variants(variants, capacity, count);
+    if (kernel != SPCONV_KERNEL_STRIDE1 && kernel != SPCONV_KERNEL_GENERIC) return SPCONV_EINVAL;
+    int n = 0;
+    auto put = [&](int a, int b, int c, int d) {
+        if (n < capacity) {
+            variants[4 * n] = a;
+            variants[4 * n + 1] = b;
+            variants[4 * n + 2] = c;
+            variants[4 * n + 3] = d;
+        }
+        ++n;
+    };
+    if (kernel == SPCONV_KERNEL_GENERIC) {
+        put(4, 0, 4, 0);
+        put(4, 0, 4, 1);
+    } else {
+        for (const S1Variant &v : kS1Variants)
+            for (int pool = 0; pool < 2; ++pool)
+                if (v.pools & (1 << pool)) put(v.pi, v.ipw, v.rpw, pool);
+    }
+    *count = n;
     return SPCONV_OK;
 }

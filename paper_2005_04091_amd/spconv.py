@@ -27,7 +27,7 @@ SPCONV_UNPADDED_INPUT = 4
 
 EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
             "spconv_output_shape", "spconv_strerror", "spconv_dense_size", "spconv_pack_dense",
-            "spconv_forward_dense", "spconv_dense_plan", "spconv_select_path")
+            "spconv_forward_dense", "spconv_dense_plan", "spconv_select_path", "spconv_kernel_variants")
 SPCONV_KERNEL_STRIDE1 = 1
 SPCONV_KERNEL_GENERIC = 2
 SPCONV_KERNEL_DENSE = 3
@@ -40,12 +40,13 @@ class spconv_csr(ctypes.Structure):
     _fields_ = [("K", ctypes.c_int32), ("C", ctypes.c_int32), ("R", ctypes.c_int32), ("S", ctypes.c_int32),
                 ("Hp", ctypes.c_int32), ("Wp", ctypes.c_int32), ("nnz", ctypes.c_int64),
                 ("rowptr", ctypes.c_void_p), ("colidx", ctypes.c_void_p), ("offset", ctypes.c_void_p),
-                ("vals", ctypes.c_void_p), ("max_row_nnz", ctypes.c_int64)]
+                ("vals", ctypes.c_void_p)]
 
 
-class spconv_epilogue(ctypes.Structure):
-    """Mirror of ``struct spconv_epilogue``."""
-    _fields_ = [("out_pad", ctypes.c_int32), ("residual_pad", ctypes.c_int32), ("residual", ctypes.c_void_p)]
+class spconv_options(ctypes.Structure):
+    """Mirror of ``struct spconv_options``."""
+    _fields_ = [("out_pad", ctypes.c_int32), ("residual_pad", ctypes.c_int32), ("residual", ctypes.c_void_p),
+                ("max_row_nnz", ctypes.c_int64)]
 
 
 class spconv_plan_info(ctypes.Structure):
@@ -76,10 +77,11 @@ def _bind(lib):
     lib.spconv_forward_ex.restype = _c_int
     lib.spconv_forward_ex.argtypes = [_vp, _c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int,
                                       _c_int, _c_int, _c_int, _c_int, _vp, ctypes.c_uint32,
-                                      ctypes.POINTER(spconv_epilogue), _vp, _vp]
+                                      ctypes.POINTER(spconv_options), _vp, _vp]
     lib.spconv_plan.restype = _c_int
     lib.spconv_plan.argtypes = [_c_int, _c_int, _c_int, _c_int, ctypes.POINTER(spconv_csr), _c_int, _c_int, _c_int,
-                                _c_int, _c_int, ctypes.c_uint32, ctypes.POINTER(spconv_plan_info)]
+                                _c_int, _c_int, ctypes.c_uint32, ctypes.POINTER(spconv_options),
+                                ctypes.POINTER(spconv_plan_info)]
     lib.spconv_output_shape.restype = _c_int
     lib.spconv_output_shape.argtypes = [_c_int, _c_int, _c_int, _c_int, _c_int, _c_int, ctypes.c_uint32,
                                         ctypes.POINTER(_c_int), ctypes.POINTER(_c_int)]
@@ -91,11 +93,13 @@ def _bind(lib):
     lib.spconv_pack_dense.argtypes = [_vp, _vp] + [_c_int] * 4 + [_vp, ctypes.c_int64]
     lib.spconv_forward_dense.restype = _c_int
     lib.spconv_forward_dense.argtypes = [_vp] + [_c_int] * 4 + [_vp] + [_c_int] * 4 + [
-        _vp, ctypes.c_uint32, ctypes.POINTER(spconv_epilogue), _vp, _vp]
+        _vp, ctypes.c_uint32, ctypes.POINTER(spconv_options), _vp, _vp]
     lib.spconv_dense_plan.restype = _c_int
     lib.spconv_dense_plan.argtypes = [_c_int] * 8 + [ctypes.c_uint32, ctypes.POINTER(spconv_plan_info)]
     lib.spconv_select_path.restype = _c_int
     lib.spconv_select_path.argtypes = [_c_int] * 9 + [ctypes.c_int64, ctypes.c_uint32, ctypes.POINTER(_c_int)]
+    lib.spconv_kernel_variants.restype = _c_int
+    lib.spconv_kernel_variants.argtypes = [ctypes.c_int32, _vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
     return lib
 
 
@@ -220,10 +224,12 @@ class DeviceCSR:
         self.colidx = torch.from_numpy(np.concatenate([host.colidx, np.zeros(1, np.int32)])).to(device)
         self.offset = torch.from_numpy(np.concatenate([host.offset, np.zeros(1, np.int32)])).to(device)
         self.vals = torch.from_numpy(np.concatenate([host.vals, np.zeros(1, np.float32)])).to(device)
-        max_row = int(np.diff(host.rowptr).max()) if host.K > 0 else 0
+        # The largest row's entry count: the planner's hint for skewed filters
+        # (passed in spconv_options; the planner never reads the device arrays).
+        self.max_row_nnz = int(np.diff(host.rowptr).max()) if host.K > 0 else 0
         self.struct = spconv_csr(host.K, host.C, host.R, host.S, host.Hp, host.Wp, host.nnz,
                                  self.rowptr.data_ptr(), self.colidx.data_ptr(), self.offset.data_ptr(),
-                                 self.vals.data_ptr(), max_row)
+                                 self.vals.data_ptr())
 
 
 def _dev_ptr(t, name):
@@ -254,23 +260,33 @@ def _in_elems(N, C, H, W, pad, flags):
     return N * C * (H + 2 * p) * (W + 2 * p)
 
 
-def _stream_handle(stream, device):
+def _stream_of(stream, device):
     import torch
-    s = stream if stream is not None else torch.cuda.current_stream(device)
-    return s.cuda_stream
+    return stream if stream is not None else torch.cuda.current_stream(device)
+
+
+def _empty(shape, device, stream):
+    """A new float32 device tensor whose memory belongs to ``stream``: torch's
+    caching allocator ties a block to the stream current at allocation, and
+    reuses it on that stream once the tensor is freed, so allocating on the
+    stream the kernels run on keeps a freed temporary from being handed out
+    while those kernels still use it."""
+    import torch
+    with torch.cuda.stream(stream):
+        return torch.empty(shape, dtype=torch.float32, device=device)
 
 
 def spconv_pad_input(x, pad: int, out=None, stream=None):
     """Zero-padded copy of NCHW ``x`` (device), queued on ``stream``."""
-    import torch
     if x.dim() != 4:
         raise ValueError("x must be NCHW")
     N, C, H, W = (int(v) for v in x.shape)
+    s = _stream_of(stream, x.device)
     if out is None:
-        out = torch.empty((N, C, H + 2 * pad, W + 2 * pad), dtype=torch.float32, device=x.device)
+        out = _empty((N, C, H + 2 * pad, W + 2 * pad), x.device, s)
     _check_shape(out, (N, C, H + 2 * pad, W + 2 * pad), "out")
-    _check(_lib.spconv_pad_input(_dev_ptr(x, "x"), N, C, H, W, pad, _dev_ptr(out, "out"),
-                                 _stream_handle(stream, x.device)), "spconv_pad_input")
+    _check(_lib.spconv_pad_input(_dev_ptr(x, "x"), N, C, H, W, pad, _dev_ptr(out, "out"), s.cuda_stream),
+           "spconv_pad_input")
     return out
 
 
@@ -278,55 +294,59 @@ def spconv_resize_pad_input(x, H: int, W: int, pad: int, out=None, stream=None):
     """Bilinear resize (pixel centres aligned) of NCHW ``x`` to H x W, written
     with a zero border of ``pad`` into ``out`` [N, C, H+2pad, W+2pad] (device),
     queued on ``stream``."""
-    import torch
     if x.dim() != 4:
         raise ValueError("x must be NCHW")
     N, C, Hin, Win = (int(v) for v in x.shape)
     shape = (N, C, H + 2 * pad, W + 2 * pad)
+    s = _stream_of(stream, x.device)
     if out is None:
-        out = torch.empty(shape, dtype=torch.float32, device=x.device)
+        out = _empty(shape, x.device, s)
     _check_shape(out, shape, "out")
     _check(_lib.spconv_resize_pad_input(_dev_ptr(x, "x"), N, C, Hin, Win, H, W, pad, _dev_ptr(out, "out"),
-                                        _stream_handle(stream, x.device)), "spconv_resize_pad_input")
+                                        s.cuda_stream), "spconv_resize_pad_input")
     return out
 
 
 def spconv_forward(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int,
                    pad: int, bias=None, flags: int = SPCONV_RELU, out=None, stream=None):
-    """Fused sparse conv + bias + ReLU (+ 2x2 max-pool) on the padded input ``xp``."""
-    import torch
+    """Fused sparse conv + bias + ReLU (+ 2x2 max-pool) on the padded input
+    ``xp``: the plain ``spconv_forward`` call (no options, so the planner does
+    not see ``csr``'s row skew)."""
     Ho, Wo = spconv_output_shape(H, W, R, S, stride, pad, flags)
+    s = _stream_of(stream, xp.device)
     if out is None:
-        out = torch.empty((N, K, Ho, Wo), dtype=torch.float32, device=xp.device)
+        out = _empty((N, K, Ho, Wo), xp.device, s)
     _check_numel(xp, _in_elems(N, C, H, W, pad, flags), "xp")
     _check_numel(out, N * K * Ho * Wo, "out")
     _check_numel(bias, K, "bias")
     _check(_lib.spconv_forward(_dev_ptr(xp, "xp"), N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad,
-                               _dev_ptr(bias, "bias"), flags, _dev_ptr(out, "out"),
-                               _stream_handle(stream, xp.device)), "spconv_forward")
+                               _dev_ptr(bias, "bias"), flags, _dev_ptr(out, "out"), s.cuda_stream),
+           "spconv_forward")
     return out
 
 
 def spconv_forward_ex(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int,
                       pad: int, bias=None, flags: int = SPCONV_RELU, out_pad: int = 0, residual=None,
-                      residual_pad: int = 0, out=None, stream=None):
-    """``spconv_forward`` with epilogue options: the stored planes get a zero
-    border of ``out_pad`` (the next layer's padded input), and ``residual`` (on
-    the convolution's grid, with a border of ``residual_pad``) is added before
-    the activation."""
-    import torch
+                      residual_pad: int = 0, out=None, stream=None, max_row_nnz: int | None = None):
+    """``spconv_forward`` with options: the stored planes get a zero border of
+    ``out_pad`` (the next layer's padded input), ``residual`` (on the
+    convolution's grid, with a border of ``residual_pad``) is added before the
+    activation, and the planner gets ``max_row_nnz`` (default: the value
+    measured on ``csr``'s host arrays; 0 = unknown)."""
     Hs, Ws = spconv_output_shape(H, W, R, S, stride, pad, flags)
+    s = _stream_of(stream, xp.device)
     if out is None:
-        out = torch.empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), dtype=torch.float32, device=xp.device)
+        out = _empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), xp.device, s)
     Hc, Wc = spconv_output_shape(H, W, R, S, stride, pad, flags & ~SPCONV_MAXPOOL2X2)
     _check_numel(xp, _in_elems(N, C, H, W, pad, flags), "xp")
     _check_numel(out, N * K * (Hs + 2 * out_pad) * (Ws + 2 * out_pad), "out")
     _check_numel(bias, K, "bias")
     _check_numel(residual, N * K * (Hc + 2 * residual_pad) * (Wc + 2 * residual_pad), "residual")
-    epi = spconv_epilogue(out_pad, residual_pad, _dev_ptr(residual, "residual"))
+    hint = csr.max_row_nnz if max_row_nnz is None else max_row_nnz
+    opt = spconv_options(out_pad, residual_pad, _dev_ptr(residual, "residual"), hint)
     _check(_lib.spconv_forward_ex(_dev_ptr(xp, "xp"), N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad,
-                                  _dev_ptr(bias, "bias"), flags, ctypes.byref(epi), _dev_ptr(out, "out"),
-                                  _stream_handle(stream, xp.device)), "spconv_forward_ex")
+                                  _dev_ptr(bias, "bias"), flags, ctypes.byref(opt), _dev_ptr(out, "out"),
+                                  s.cuda_stream), "spconv_forward_ex")
     return out
 
 
@@ -335,31 +355,48 @@ def spconv_forward_dense(xp, N: int, C: int, H: int, W: int, packed, K: int, R: 
                          stream=None):
     """The fused conv of ``spconv_forward_ex`` from the packed dense filter
     ``packed`` (device), stride 1."""
-    import torch
     Hs, Ws = spconv_output_shape(H, W, R, S, 1, pad, flags)
+    s = _stream_of(stream, xp.device)
     if out is None:
-        out = torch.empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), dtype=torch.float32, device=xp.device)
+        out = _empty((N, K, Hs + 2 * out_pad, Ws + 2 * out_pad), xp.device, s)
     Hc, Wc = spconv_output_shape(H, W, R, S, 1, pad, flags & ~SPCONV_MAXPOOL2X2)
     _check_numel(xp, _in_elems(N, C, H, W, pad, flags), "xp")
     _check_numel(packed, spconv_dense_size(K, C, R, S), "packed")
     _check_numel(out, N * K * (Hs + 2 * out_pad) * (Ws + 2 * out_pad), "out")
     _check_numel(bias, K, "bias")
     _check_numel(residual, N * K * (Hc + 2 * residual_pad) * (Wc + 2 * residual_pad), "residual")
-    epi = spconv_epilogue(out_pad, residual_pad, _dev_ptr(residual, "residual"))
+    opt = spconv_options(out_pad, residual_pad, _dev_ptr(residual, "residual"), 0)
     _check(_lib.spconv_forward_dense(_dev_ptr(xp, "xp"), N, C, H, W, _dev_ptr(packed, "packed"), K, R, S, pad,
-                                     _dev_ptr(bias, "bias"), flags, ctypes.byref(epi), _dev_ptr(out, "out"),
-                                     _stream_handle(stream, xp.device)), "spconv_forward_dense")
+                                     _dev_ptr(bias, "bias"), flags, ctypes.byref(opt), _dev_ptr(out, "out"),
+                                     s.cuda_stream), "spconv_forward_dense")
     return out
 
 
-def spconv_plan(N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int, pad: int,
-                flags: int = SPCONV_RELU) -> dict:
-    """The launch plan ``spconv_forward`` would use, as a dict of the
-    ``spconv_plan_info`` fields."""
+def spconv_plan(N: int, C: int, H: int, W: int, csr, K: int, R: int, S: int, stride: int, pad: int,
+                flags: int = SPCONV_RELU, max_row_nnz: int | None = None) -> dict:
+    """The launch plan ``spconv_forward_ex`` would use, as a dict of the
+    ``spconv_plan_info`` fields. ``csr`` is a DeviceCSR (its arrays are not
+    read; the hint defaults to its measured max_row_nnz) or a bare
+    ``spconv_csr`` struct (hint default 0)."""
+    struct = csr.struct if isinstance(csr, DeviceCSR) else csr
+    if max_row_nnz is None:
+        max_row_nnz = csr.max_row_nnz if isinstance(csr, DeviceCSR) else 0
+    opt = spconv_options(0, 0, None, max_row_nnz)
     info = spconv_plan_info()
-    _check(_lib.spconv_plan(N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad, flags, ctypes.byref(info)),
-           "spconv_plan")
+    _check(_lib.spconv_plan(N, C, H, W, ctypes.byref(struct), K, R, S, stride, pad, flags, ctypes.byref(opt),
+                            ctypes.byref(info)), "spconv_plan")
     return {name: getattr(info, name) for name, _ in spconv_plan_info._fields_}
+
+
+def spconv_kernel_variants(kernel: int) -> list:
+    """The compiled instances of a kernel family, as 4-tuples (see
+    ``spconv_kernel_variants`` in include/spconv.h)."""
+    count = ctypes.c_int32()
+    _check(_lib.spconv_kernel_variants(kernel, None, 0, ctypes.byref(count)), "spconv_kernel_variants (count)")
+    buf = np.zeros(4 * max(count.value, 1), np.int32)
+    _check(_lib.spconv_kernel_variants(kernel, _np_ptr(buf), count.value, ctypes.byref(count)),
+           "spconv_kernel_variants")
+    return [tuple(int(v) for v in buf[4 * i:4 * i + 4]) for i in range(count.value)]
 
 
 def flags_of(relu: bool, pool: bool) -> int:
@@ -419,9 +456,8 @@ class SparseConvLayer:
             return spconv_forward_dense(xp, N, self.C, self.H, self.W, self.dense, self.K, self.R, self.S, self.pad,
                                         self.bias, flags, out_pad=out_pad, residual=residual,
                                         residual_pad=residual_pad, out=out, stream=stream)
-        if out_pad == 0 and residual is None:
-            return spconv_forward(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
-                                  self.pad, self.bias, flags, out=out, stream=stream)
+        # Through spconv_forward_ex, so that the planner sees the filter's row
+        # skew (max_row_nnz) whatever the epilogue.
         return spconv_forward_ex(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
                                  self.pad, self.bias, flags, out_pad=out_pad, residual=residual,
                                  residual_pad=residual_pad, out=out, stream=stream)

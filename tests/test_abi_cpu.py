@@ -36,7 +36,7 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted(
         ["spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "spconv_forward", "spconv_forward_ex",
          "spconv_plan", "spconv_dense_size", "spconv_pack_dense", "spconv_forward_dense", "spconv_dense_plan",
-         "spconv_select_path",
+         "spconv_select_path", "spconv_kernel_variants",
          "spconv_output_shape", "spconv_strerror"])
 
 
@@ -186,18 +186,19 @@ def test_forward_and_pad_validate_before_any_gpu_work(sp):
     assert fwd(csr=bad_nnz) == E
     null_rows = sp.spconv_csr(4, 3, 3, 3, 10, 12, 5, None, fake, fake, fake)
     assert fwd(csr=null_rows) == E
-    for bad_hint in (-1, 6):        # the largest row cannot have more entries than the filter
-        assert fwd(csr=sp.spconv_csr(4, 3, 3, 3, 10, 12, 5, fake, fake, fake, fake, bad_hint)) == E
     tiny = sp.spconv_csr(4, 3, 3, 3, 3, 3, 5, fake, fake, fake, fake)
     assert fwd(csr=tiny, H=3, W=3, pad=0, flags=sp.SPCONV_MAXPOOL2X2) == E  # 1x1 output cannot be pooled
     # epilogue options are checked on the host as well
-    def fwd_ex(out_pad=0, residual_pad=0, residual=None, **kw):
+    def fwd_ex(out_pad=0, residual_pad=0, residual=None, max_row_nnz=0, **kw):
         a = dict(ok)
         a.update(kw)
-        epi = sp.spconv_epilogue(out_pad, residual_pad, residual)
+        opt = sp.spconv_options(out_pad, residual_pad, residual, max_row_nnz)
         return lib.spconv_forward_ex(a["xp"], a["N"], a["C"], a["H"], a["W"], ctypes.byref(csr), a["K"], a["R"],
-                                     a["S"], a["stride"], a["pad"], a["bias"], a["flags"], ctypes.byref(epi),
+                                     a["S"], a["stride"], a["pad"], a["bias"], a["flags"], ctypes.byref(opt),
                                      a["out"], None)
+
+    for bad_hint in (-1, 6):        # the largest row cannot have more entries than the filter
+        assert fwd_ex(max_row_nnz=bad_hint) == E
 
     assert fwd_ex(out_pad=-1) == E
     assert fwd_ex(residual=fake, residual_pad=-1) == E
@@ -232,9 +233,11 @@ def test_plan_reports_the_launch_without_a_gpu(sp):
 
     def plan(N, C, H, W, K, R=3, S=3, stride=1, pad=1, flags=sp.SPCONV_RELU, nnz=None, max_row=0):
         nnz = int(0.2 * K * C * R * S) if nnz is None else nnz
-        csr = sp.spconv_csr(K, C, R, S, H + 2 * pad, W + 2 * pad, nnz, fake, fake, fake, fake, max_row)
+        csr = sp.spconv_csr(K, C, R, S, H + 2 * pad, W + 2 * pad, nnz, fake, fake, fake, fake)
+        opt = sp.spconv_options(0, 0, None, max_row)
         info = sp.spconv_plan_info()
-        rc = lib.spconv_plan(N, C, H, W, ctypes.byref(csr), K, R, S, stride, pad, flags, ctypes.byref(info))
+        rc = lib.spconv_plan(N, C, H, W, ctypes.byref(csr), K, R, S, stride, pad, flags, ctypes.byref(opt),
+                             ctypes.byref(info))
         return rc, info
 
     rc, p = plan(32, 64, 56, 56, 64)                      # ResNet-style layer
@@ -254,8 +257,14 @@ def test_plan_reports_the_launch_without_a_gpu(sp):
     assert rc == sp.SPCONV_OK and p.kernel == sp.SPCONV_KERNEL_GENERIC
     assert plan(2, 5, 9, 8, 7, max_row=10 ** 9)[0] == sp.SPCONV_EINVAL  # hint above nnz
     assert plan(2, 5, 9, 8, 7, flags=8)[0] == sp.SPCONV_EINVAL
-    csr = sp.spconv_csr(7, 5, 3, 3, 11, 10, 60, fake, fake, fake, fake, 0)
-    assert lib.spconv_plan(2, 5, 9, 8, ctypes.byref(csr), 7, 3, 3, 1, 1, 1, None) == sp.SPCONV_EINVAL
+    csr = sp.spconv_csr(7, 5, 3, 3, 11, 10, 60, fake, fake, fake, fake)
+    assert lib.spconv_plan(2, 5, 9, 8, ctypes.byref(csr), 7, 3, 3, 1, 1, 1, None, None) == sp.SPCONV_EINVAL
+    # options are optional: NULL plans like a zero struct
+    info = sp.spconv_plan_info()
+    assert lib.spconv_plan(2, 5, 9, 8, ctypes.byref(csr), 7, 3, 3, 1, 1, 1, None, ctypes.byref(info)) == sp.SPCONV_OK
+    opt = sp.spconv_options(-1, 0, None, 0)
+    assert lib.spconv_plan(2, 5, 9, 8, ctypes.byref(csr), 7, 3, 3, 1, 1, 1, ctypes.byref(opt),
+                           ctypes.byref(info)) == sp.SPCONV_EINVAL
 
 
 def test_plans_fit_the_lds_over_a_sweep_of_shapes(sp):
@@ -273,9 +282,10 @@ def test_plans_fit_the_lds_over_a_sweep_of_shapes(sp):
                     flags = sp.SPCONV_RELU | (sp.SPCONV_MAXPOOL2X2 if pool else 0)
                     K = 64
                     nnz = max(1, int(0.2 * K * C * 9))
-                    csr = sp.spconv_csr(K, C, 3, 3, H + 2, W + 2, nnz, fake, fake, fake, fake, 0)
+                    csr = sp.spconv_csr(K, C, 3, 3, H + 2, W + 2, nnz, fake, fake, fake, fake)
                     info = sp.spconv_plan_info()
-                    rc = lib.spconv_plan(N, C, H, W, ctypes.byref(csr), K, 3, 3, 1, 1, flags, ctypes.byref(info))
+                    rc = lib.spconv_plan(N, C, H, W, ctypes.byref(csr), K, 3, 3, 1, 1, flags, None,
+                                         ctypes.byref(info))
                     if rc != sp.SPCONV_OK:
                         continue
                     seen += 1

@@ -84,8 +84,8 @@ def test_forward_dense_validates_before_any_gpu_work(sp):
     assert call(R=3, S=1) == E
     assert call(H=1, W=1, flags=3) == E                # pool of a 1x1 output
     assert call(W=224, flags=3) == E                   # pool tile wider than 8 blocks
-    assert call(epi=sp.spconv_epilogue(-1, 0, None)) == E
-    assert call(epi=sp.spconv_epilogue(0, -1, fake)) == E
+    assert call(epi=sp.spconv_options(-1, 0, None, 0)) == E
+    assert call(epi=sp.spconv_options(0, -1, fake, 0)) == E
     info = sp.spconv_plan_info()
     assert lib.spconv_dense_plan(2, 4, 8, 8, 8, 3, 3, 1, 1, None) == E
     assert lib.spconv_dense_plan(2, 4, 8, 8, 8, 3, 3, 1, 1, ctypes.byref(info)) == sp.SPCONV_OK

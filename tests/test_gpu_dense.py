@@ -102,10 +102,10 @@ def test_dense_out_pad_bitwise(sp, i):
     assert np.array_equal(buf.cpu().numpy().view(np.uint32), ref.view(np.uint32))
 
 
-def test_dense_full_size_narrow_sampled(sp):
+def test_dense_full_size_narrow(sp):
     """The deep narrow layer at density 0.5 (32 x 256 x 14x14, Beta(2,5) row
-    skew) in the plan the benchmark runs: sampled (image, channel) planes
-    against the oracle, and the dispatcher's choice for it."""
+    skew) in the plan the benchmark runs, whole output tensor against the
+    oracle, and the dispatcher's choice for it."""
     import torch
     layer = synth.make_layer("narrow_d0.5")
     N, C, H, W, K, R, S = layer.shape
@@ -114,12 +114,8 @@ def test_dense_full_size_narrow_sampled(sp):
     say("dense narrow_d0.5 full size", L.plan(N))
     out = L.run(torch.from_numpy(layer.x).cuda())
     torch.cuda.synchronize()
-    got = out.cpu().numpy()
-    rng = np.random.default_rng(3)
-    pairs = [(0, 0), (N - 1, K - 1)] + [(int(rng.integers(N)), int(rng.integers(K))) for _ in range(40)]
-    ref, ab = oracle.conv(layer.x, layer.w, layer.mask, layer.bias, 1, 1, True, False, pairs=pairs)
-    for j, (n, k) in enumerate(pairs):
-        check_close(got[n, k], ref[j], ab[j], f"narrow pair {(n, k)}")
+    ref, ab = oracle.conv(layer.x, layer.w, layer.mask, layer.bias, 1, 1, True, False)
+    check_close(out.cpu().numpy(), ref, ab, "narrow_d0.5 dense")
 
 
 def test_dense_and_sparse_agree(sp):

@@ -151,11 +151,11 @@ def test_resize_conv_relu_maxpool_block(sp, case):
     assert (err2 <= _block_tol(layer, ab2, float(np.abs(src).max()))).all(), f"end to end: max err {err2.max():.3e}"
 
 
-def test_resize_block_full_size_sampled(sp):
+def test_resize_block_full_size(sp):
     """The benchmarked block at full size (32 x 128 x 42x42 -> 28x28, conv,
     ReLU, 2x2 max-pool), in the launch configuration the benchmark times: the
-    whole resized tensor against the oracle, and the block output of sampled
-    (image, channel) planes end to end."""
+    whole resized tensor against the oracle, and the whole block output end
+    to end."""
     import torch
     src, layer = synth.make_resize_block()
     N, C, H, W, K, R, S = layer.shape
@@ -166,12 +166,8 @@ def test_resize_block_full_size_sampled(sp):
     torch.cuda.synchronize()
     check_resize(xp.cpu().numpy(), src, H, W, 1, "full-size resize")
     got = out.cpu().numpy().astype(np.float64)
-    rng = np.random.default_rng(11)
-    pairs = [(0, 0), (N - 1, K - 1)] + [(int(rng.integers(N)), int(rng.integers(K))) for _ in range(30)]
     rs, _ = oracle.resize(src, H, W)
-    ref, ab = oracle.conv(rs.astype(np.float32), layer.w, layer.mask, layer.bias, 1, 1, True, True, pairs=pairs)
-    wsum = np.abs(layer.w.astype(np.float64)).reshape(K, -1).sum(axis=1)
-    for j, (n, k) in enumerate(pairs):
-        tol = REL_TOL * ab[j] + ABS_TOL + 2.0 * RESIZE_TOL * float(np.abs(src).max()) * wsum[k]
-        err = np.abs(got[n, k] - ref[j])
-        assert (err <= tol).all(), f"pair {(n, k)}: max err {err.max():.3e}"
+    ref, ab = oracle.conv(rs.astype(np.float32), layer.w, layer.mask, layer.bias, 1, 1, True, True)
+    err = np.abs(got - ref)
+    tol = _block_tol(layer, ab, float(np.abs(src).max()))
+    assert (err <= tol).all(), f"end to end: {int((err > tol).sum())} outputs out of bound, max err {err.max():.3e}"

@@ -117,9 +117,9 @@ def test_stride2_pads_first_and_flag_is_rejected(sp):
     tp.check_close(out.cpu().numpy(), ref, ab, "stride 2")
 
 
-def test_unpadded_resnet_full_size_sampled(sp):
-    """The benchmarked ResNet layer through the fused-pad forward, against the
-    oracle on sampled planes."""
+def test_unpadded_resnet_full_size(sp):
+    """The benchmarked ResNet layer through the fused-pad forward, whole output
+    tensor against the oracle."""
     import torch
     layer = synth.make_layer("resnet")
     N, C, H, W, K, R, S = layer.shape
@@ -127,11 +127,8 @@ def test_unpadded_resnet_full_size_sampled(sp):
     say("unpadded resnet", L.path, L.plan(N))
     out = L.forward(torch.from_numpy(layer.x).cuda(), pad_in_kernel=True)
     torch.cuda.synchronize()
-    got = out.cpu().numpy()
-    pairs = [(0, 0), (31, 63), (7, 13), (19, 40), (25, 1)]
-    ref, ab = oracle.conv(layer.x, layer.w, layer.mask, layer.bias, 1, 1, True, False, pairs=pairs)
-    for j, (n, k) in enumerate(pairs):
-        tp.check_close(got[n, k], ref[j], ab[j], f"pair {(n, k)}")
+    ref, ab = oracle.conv(layer.x, layer.w, layer.mask, layer.bias, 1, 1, True, False)
+    tp.check_close(out.cpu().numpy(), ref, ab, "unpadded resnet")
 
 
 def test_resnet_block_without_pad_passes_bitwise(sp):
