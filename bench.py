@@ -1,12 +1,20 @@
 """Benchmark of the fused sparse convolution on one MI355X.
 
-One step = the whole hot path on one batch: zero-pad the NCHW input, then the
-fused sparse conv + bias + ReLU (+ 2x2 max-pool). Where the kernel forms the
-zero border while staging its input (SPCONV_UNPADDED_INPUT) that is one
-launch; otherwise spconv_pad_input, then spconv_forward. Inputs are seeded synthetic layers already resident in HBM.
-Prints one JSON line (rank 0) with the throughput in nonzero GFLOP/s, ms/layer,
-the fraction of the HBM roofline, a roofline record for the dominant kernel and
-the CPU oracle's rate on the same workload.
+Default workload: the VGG-style block (N=32, 224x224, C=K=64 with 3 real input
+channels, two chained 3x3 sparse convs at density 0.2 with fused bias + ReLU,
+the second with a fused 2x2 max-pool to 112x112), the largest layer
+configuration. One step = the whole hot path on one resident batch: layer 1
+forms its input's zero border while staging it in LDS and writes layer 2's
+zero-bordered input; layer 2 adds the max-pool. The JSON line (rank 0) carries
+the block's nonzero GFLOP/s, ms per step, per-layer times (HIP events on the
+launch stream inside the timed steps, and the median of 30 runs each after a
+512 MiB write that flushes the last-level cache), a roofline record for the
+dominant kernel, the CPU oracle's rate on the same block, and a `per_config`
+list with the same measurements for the other layer configurations (the tiny,
+ResNet, conv+pool and deep narrow layers).
+
+`--workload NAME` times one other layer or block instead (old single-layer
+record), for profiling.
 """
 from __future__ import annotations
 
@@ -137,23 +145,46 @@ def cold_median_ms(fn, stream, reps: int, dev) -> float:
 
 
 def measured_copy_gbs(dev) -> float:
-    """Device-to-device copy rate of a 512 MiB buffer (read + write bytes per
-    second, best of 5): the practical HBM ceiling beside the 8 TB/s spec."""
+    """Device-to-device copy rate of a 512 MiB tensor through the library's
+    pad kernel with pad 0 (a 16-byte-per-lane streaming copy), read + write
+    bytes per second, best of 5: the practical HBM ceiling beside the 8 TB/s
+    spec."""
     import torch
+    from paper_2005_04091_amd import spconv
     n = 512 * 1024 * 1024 // 4
-    src = torch.ones(n, dtype=torch.float32, device=dev)
+    src = torch.ones((1, 1, 8192, n // 8192), dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream(dev)
     best = None
     for _ in range(6):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        dst.copy_(src)
-        e1.record()
+        e0.record(stream)
+        spconv.spconv_pad_input(src, 0, out=dst, stream=stream)
+        e1.record(stream)
         torch.cuda.synchronize()
         t = e0.elapsed_time(e1)
         best = t if best is None else min(best, t)
     del src, dst
     return 2.0 * n * 4 / (best * 1e-3) / 1e9
+
+
+def roof(flops, nbytes, ms, peak_tflops):
+    """Roofline figures of one launch: fraction of the HBM peak and of the
+    arithmetic peak achieved; the most HBM fraction the layer can show at all
+    (its bytes over the time of the binding roof: below 1 when the arithmetic
+    peak binds first); and the fraction of that binding roof achieved."""
+    t = ms * 1e-3
+    t_hbm = nbytes / (HBM_PEAK_GBS * 1e9)
+    t_alu = flops / (peak_tflops * 1e12)
+    t_min = max(t_hbm, t_alu)
+    return {
+        "hbm_frac": round(nbytes / t / 1e9 / HBM_PEAK_GBS, 4),
+        "compute_frac": round(flops / t / 1e12 / peak_tflops, 4),
+        "compute_peak_tflops": peak_tflops,
+        "max_hbm_frac_at_compute_peak": round(t_hbm / t_min, 4),
+        "binding_roof": "hbm" if t_hbm >= t_alu else "compute",
+        "binding_roof_frac": round(t_min / t, 4),
+    }
 
 
 def cpu_baseline(layer, budget_s: float, nthreads: int = 0):
@@ -392,14 +423,289 @@ def bench_resize_block(args, dev):
     print(json.dumps(rec), flush=True)
 
 
+METRIC = "ms/layer + nonzero GFLOP/s + % HBM roofline, fused sparse conv, 1 MI355X"
+DATA = "synthetic (seeded Bernoulli-masked weights U[-1,1), input U[0,1), bias U[-0.1,0.1))"
+COLD_REPS = 30  # the paper reports the median of 30 runs
+
+
+def layer_launch(L, x, out, stream, xp=None):
+    """The forward of one layer on a resident batch, as the step runs it: one
+    launch on the unpadded input when the kernel forms the zero border while
+    staging (wide rows), else the forward on an already padded copy `xp`."""
+    N = int(x.shape[0])
+    if L.pads_in_kernel(N):
+        return lambda: L.forward(x, out=out, stream=stream)
+    return lambda: L.forward_padded(xp, out=out, stream=stream)
+
+
+def per_config_record(name, args, dev, stream):
+    """One of the other layer configurations, measured like the block's layers:
+    back-to-back launches (warm), the cold median of 30 of the forward alone and
+    of pad + forward, nonzero GFLOP/s, and the roofline figures against HBM and
+    the arithmetic peak of the path that runs (v_fma_f32 for the sparse kernels,
+    the fp32 matrix cores for the dense one)."""
+    import torch
+    from paper_2005_04091_amd import spconv, synth
+    layer = synth.make_layer(name)
+    N, C, H, W, K, R, S = layer.shape
+    L = spconv.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, layer.stride, layer.pad, layer.relu,
+                               layer.pool, device=dev, path="auto", N=N)
+    x = torch.from_numpy(layer.x).to(dev)
+    xp = torch.empty((N, C, H + 2 * layer.pad, W + 2 * layer.pad), dtype=torch.float32, device=dev)
+    out = torch.empty((N, K, L.Ho, L.Wo), dtype=torch.float32, device=dev)
+    fused_pad = L.pads_in_kernel(N)
+    if not fused_pad:
+        L.pad_input(x, out=xp, stream=stream)
+    fwd = layer_launch(L, x, out, stream, xp)
+
+    def step():
+        if not fused_pad:
+            L.pad_input(x, out=xp, stream=stream)
+        fwd()
+
+    ms_warm = _timed(args, stream, fwd)
+    ms_cold = cold_median_ms(fwd, stream, COLD_REPS, dev)
+    ms_step_cold = cold_median_ms(step, stream, COLD_REPS, dev)
+    nnz = L.host_csr.nnz
+    flops, nbytes, _ = algorithmic(layer, nnz)
+    if fused_pad:
+        nbytes -= 4.0 * N * C * ((H + 2 * layer.pad) * (W + 2 * layer.pad) - H * W)
+    rec = {"workload": name, "description": WORKLOADS[name], "path": L.path, "nnz": nnz,
+           "density": round(nnz / (K * C * R * S), 5), "pad": "in the kernel" if fused_pad else "separate pass",
+           "plan": L.plan(N),
+           "ms_per_layer": round(ms_cold, 5), "ms_per_layer_warm": round(ms_warm, 5),
+           "ms_per_layer_with_pad": round(ms_step_cold, 5),
+           "nonzero_gflops": round(flops / (ms_cold * 1e-3) / 1e9, 1),
+           "nonzero_gflops_warm": round(flops / (ms_warm * 1e-3) / 1e9, 1),
+           "algorithmic_bytes": int(nbytes), "nonzero_flops": flops}
+    if L.path == "dense":
+        dflops = 2.0 * K * C * R * S * N * L.Ho * L.Wo
+        nbytes_d = nbytes + 4.0 * L.dense.numel() - 8.0 * nnz
+        rec["roof"] = roof(dflops, nbytes_d, ms_cold, MFMA_FP32_TFLOPS)
+        rec["roof"]["flops_counted"] = "dense filter work on the fp32 matrix cores"
+        rec["nonzero_flops_roof"] = roof(flops, nbytes, ms_cold, VALU_FP32_FMA_TFLOPS)
+    else:
+        rec["roof"] = roof(flops, nbytes, ms_cold, VALU_FP32_FMA_TFLOPS)
+        rec["roof"]["flops_counted"] = "nonzero multiply-adds on v_fma_f32"
+    return rec
+
+
+def cpu_baseline_block(layers, budget_s: float):
+    """The CPU oracle (as it stands) on the block's two layers: whole-block
+    passes repeated while they fit the budget (median pass), else the same
+    random share of output planes of each layer. Layer 2 runs on its own
+    seeded input of the block's shape (the oracle's cost does not depend on
+    the values)."""
+    import numpy as np
+    import oracle
+    orc = oracle.get()
+    threads = orc.max_threads()
+    rng = np.random.default_rng(0)
+    per = []
+    for layer in layers:
+        N, C, H, W, K, R, S = layer.shape
+        probe = max(threads, 8)
+        pairs = [(int(p // K), int(p % K)) for p in rng.permutation(N * K)[:probe]]
+        t0 = time.perf_counter()
+        orc.conv(layer.x, layer.w, layer.mask, layer.bias, layer.stride, layer.pad, layer.relu, layer.pool, pairs=pairs)
+        per.append((time.perf_counter() - t0) / probe)
+    whole = sum(pp * l.shape[0] * l.shape[4] for pp, l in zip(per, layers))
+    row_nnz = [(l.mask.reshape(l.shape[4], -1) != 0).sum(1) for l in layers]
+
+    def flops_of(layer, rn, pairs):
+        N, C, H, W, K, R, S = layer.shape
+        if pairs is None:
+            return 2.0 * float(rn.sum()) * N * H * W
+        return sum(2.0 * rn[k] * H * W for _, k in pairs)
+
+    if whole <= budget_s / 2:
+        times = []
+        while sum(times) < budget_s or not times:
+            t0 = time.perf_counter()
+            for layer in layers:
+                orc.conv(layer.x, layer.w, layer.mask, layer.bias, layer.stride, layer.pad, layer.relu, layer.pool)
+            times.append(time.perf_counter() - t0)
+        dt = statistics.median(times)
+        flops = sum(flops_of(l, rn, None) for l, rn in zip(layers, row_nnz))
+        sample = f"the whole block (both layers), {len(times)} passes, median pass {dt:.2f} s"
+    else:
+        share = budget_s / whole
+        dt = 0.0
+        flops = 0.0
+        planes = 0
+        for layer, rn in zip(layers, row_nnz):
+            N, K = layer.shape[0], layer.shape[4]
+            count = max(threads, int(share * N * K))
+            pairs = [(int(p // K), int(p % K)) for p in rng.permutation(N * K)[:count]]
+            t0 = time.perf_counter()
+            orc.conv(layer.x, layer.w, layer.mask, layer.bias, layer.stride, layer.pad, layer.relu, layer.pool,
+                     pairs=pairs)
+            dt += time.perf_counter() - t0
+            flops += flops_of(layer, rn, pairs)
+            planes += count
+        sample = (f"{planes} random output planes (n, k) of the block's two layers "
+                  f"({100 * share:.0f}% of each), {dt:.1f} s")
+    return {"value": round(flops / dt / 1e9, 3), "unit": "GFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": sample}
+
+
+def bench_vgg(args, dev):
+    """The VGG-style block, the default workload (see the module docstring)."""
+    import torch
+    from paper_2005_04091_amd import spconv, synth
+
+    x, l1, l2 = synth.make_vgg_block()
+    N, C, H, W, K, R, S = l1.shape
+    print(f"[bench] VGG block N={N} C={C} K={K} {H}x{W}", file=sys.stderr, flush=True)
+    L1 = spconv.SparseConvLayer(l1.w, l1.mask, l1.bias, H, W, 1, 1, True, False, device=dev)
+    L2 = spconv.SparseConvLayer(l2.w, l2.mask, l2.bias, H, W, 1, 1, True, True, device=dev)
+    assert L1.path == L2.path == "sparse"
+    xd = torch.from_numpy(x).to(dev)
+    xp = torch.empty((N, C, H + 2, W + 2), dtype=torch.float32, device=dev)
+    y1p = torch.empty((N, K, H + 2, W + 2), dtype=torch.float32, device=dev)
+    y2 = torch.empty((N, K, L2.Ho, L2.Wo), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    in_kernel = L1.pads_in_kernel(N)
+    if not in_kernel:
+        L1.pad_input(xd, out=xp, stream=stream)
+    plans = [L1.plan(N), L2.plan(N)]
+    print(f"[bench] plans {plans}, layer 1 pads in the kernel: {in_kernel}", file=sys.stderr, flush=True)
+
+    def conv1():
+        if in_kernel:
+            L1.forward(xd, out=y1p, stream=stream, out_pad=1)
+        else:
+            L1.forward_padded(xp, out=y1p, stream=stream, out_pad=1)
+
+    def conv2():
+        L2.forward_padded(y1p, out=y2, stream=stream)
+
+    def step():
+        if not in_kernel:
+            L1.pad_input(xd, out=xp, stream=stream)
+        conv1()
+        conv2()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # Timed steps: an event pair around the K steps, and events around each
+    # kernel of each step on the launch stream (the per-kernel durations the
+    # roofline uses).
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for i in range(args.steps):
+        if not in_kernel:
+            L1.pad_input(xd, out=xp, stream=stream)
+        ev[i][0].record(stream)
+        conv1()
+        ev[i][1].record(stream)
+        conv2()
+        ev[i][2].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+    ms1 = statistics.mean(e[0].elapsed_time(e[1]) for e in ev)
+    ms2 = statistics.mean(e[1].elapsed_time(e[2]) for e in ev)
+    print(f"[bench] step {ms_per_step:.4f} ms, conv1 {ms1:.4f} ms, conv2+pool {ms2:.4f} ms", file=sys.stderr,
+          flush=True)
+    cold1 = cold_median_ms(conv1, stream, COLD_REPS, dev)
+    cold2 = cold_median_ms(conv2, stream, COLD_REPS, dev)
+    copy_gbs = measured_copy_gbs(dev)
+
+    nnz1, nnz2 = L1.host_csr.nnz, L2.host_csr.nnz
+    f1, b1, _ = algorithmic(l1, nnz1)
+    f2, b2, _ = algorithmic(l2, nnz2)
+    if in_kernel:  # layer 1 reads the unpadded input
+        b1 -= 4.0 * N * C * ((H + 2) * (W + 2) - H * W)
+    b1 += 4.0 * N * K * ((H + 2) * (W + 2) - H * W)  # it also writes layer 2's zero border
+    flops = f1 + f2
+    layers = {
+        "conv1": {"ms_per_layer": round(cold1, 5), "ms_in_step": round(ms1, 5), "nnz": nnz1, "plan": plans[0],
+                  "nonzero_gflops": round(f1 / (cold1 * 1e-3) / 1e9, 1), "algorithmic_bytes": int(b1),
+                  "nonzero_flops": f1, "roof": roof(f1, b1, cold1, VALU_FP32_FMA_TFLOPS),
+                  "pad": "formed in the kernel while staging" if in_kernel else "separate pass"},
+        "conv2_pool": {"ms_per_layer": round(cold2, 5), "ms_in_step": round(ms2, 5), "nnz": nnz2, "plan": plans[1],
+                       "nonzero_gflops": round(f2 / (cold2 * 1e-3) / 1e9, 1), "algorithmic_bytes": int(b2),
+                       "nonzero_flops": f2, "roof": roof(f2, b2, cold2, VALU_FP32_FMA_TFLOPS),
+                       "pad": "its input is layer 1's zero-bordered output"},
+    }
+    dom, fd, bd, msd = ("conv1", f1, b1, ms1) if ms1 >= ms2 else ("conv2_pool", f2, b2, ms2)
+    achieved = fd / (msd * 1e-3) / 1e12
+    inst = layers[dom]["plan"]
+    kname = (f"spconv_s1_kernel<{inst['pixels_per_lane']}, {inst['images_per_group']}, "
+             f"{inst['channels_per_wave']}, {'true' if dom == 'conv2_pool' else 'false'}>")
+    traffic = measured_traffic(f"vgg_{dom}", "fwd")
+    rec = {
+        "metric": METRIC,
+        "value": round(flops / (ms_per_step * 1e-3) / 1e9, 2),
+        "unit": "GFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": DATA + "; channels 3..63 of the block input are zero",
+        "config": {"workload": BLOCKS["vgg_block"], "N": N, "C": C, "K": K, "H": H, "W": W, "R": R, "S": S,
+                   "nnz": [nnz1, nnz2], "density": 0.2, "pool": "layer 2", "path": "sparse"},
+        "ms_per_layer": {k: v["ms_per_layer"] for k, v in layers.items()},
+        "ms_per_layer_protocol": f"median of {COLD_REPS} runs, each after a 512 MiB write that flushes the "
+                                 "last-level cache; HIP events around the forward alone",
+        "layers": layers,
+        "hbm_copy_measured_GBs": round(copy_gbs, 1),
+        "roofline": {
+            "kernel": kname,
+            "layer": dom,
+            "bound": "alu",
+            "achieved": round(achieved, 3),
+            "peak": VALU_FP32_FMA_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / VALU_FP32_FMA_TFLOPS, 4),
+            "traffic": traffic,
+            "traffic_source": f"profiles/spconv_fwd_vgg_{dom}_traffic.json (counter runs, source hash checked)"
+                              if traffic is not None else None,
+            "algorithmic_bytes": int(bd),
+            "flops": fd,
+            "ms_per_launch": round(msd, 5),
+            "timing": "HIP events on the launch stream around this kernel in each timed step, mean",
+        },
+        "hbm_bar": {
+            "target_frac": 0.5,
+            "note": "at 78.6 TFLOP/s (v_fma_f32, packed FP32 disabled) a layer of F nonzero FLOPs and B bytes "
+                    "cannot take less than F/78.6 TF, so its HBM fraction is at most (B/8 TB/s)/(F/78.6 TF)",
+            "max_hbm_frac_at_fma_peak": {k: v["roof"]["max_hbm_frac_at_compute_peak"] for k, v in layers.items()},
+        },
+    }
+    if not args.no_per_config:
+        pc = []
+        for name in ("tiny", "resnet", "conv_pool", "narrow_d0.05", "narrow_d0.2", "narrow_d0.5"):
+            print(f"[bench] per-config {name}", file=sys.stderr, flush=True)
+            pc.append(per_config_record(name, args, dev, stream))
+        rec["per_config"] = pc
+        rec["hbm_bar"]["max_hbm_frac_at_fma_peak"].update(
+            {r["workload"]: r["roof"]["max_hbm_frac_at_compute_peak"] for r in pc})
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on the block", file=sys.stderr, flush=True)
+        rec["cpu_baseline"] = cpu_baseline_block([l1, l2], args.cpu_budget)
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="resnet", choices=sorted(WORKLOADS) + sorted(BLOCKS))
-    ap.add_argument("--cpu-budget", type=float, default=10.0, help="seconds of oracle work for cpu_baseline")
+    ap.add_argument("--workload", default="vgg_block", choices=sorted(WORKLOADS) + sorted(BLOCKS),
+                    help="vgg_block (default): the chained VGG block with per-config records; with --compare, "
+                         "its fused and unfused variants instead; other names: one layer or block")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="default workload only: leave out the per-config records of the other layers")
     ap.add_argument("--cold", action="store_true",
                     help="also report the forward's median over 30 runs with the last-level cache flushed before each")
     ap.add_argument("--compare", action="store_true",
@@ -423,6 +729,9 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.workload == "vgg_block" and not args.compare:
+        bench_vgg(args, dev)
+        return
     if args.workload in BLOCKS:
         bench_block(args, dev)
         return
