@@ -196,6 +196,15 @@ int spconv_forward(const float *in_padded, int N, int C, int H, int W, const spc
  *           light output channels on one wave pays. It only steers the choice
  *           of tiling: results do not depend on it. Must lie in [0, nnz]
  *           (spconv_forward_dense ignores it).
+ * lowered  nullable, device: the filter as the entry stream spconv_pack_lowered
+ *           writes for this very call (same N, C, H, W, K, R, S, stride, pad,
+ *           flags and max_row_nnz), 16-byte aligned. With it the stride-1
+ *           kernel reads its entries ready-made, with scalar loads, instead of
+ *           decoding the CSR rows itself (same results bit for bit);
+ *           csr->offset and csr->vals are then not read. Calls whose plan is
+ *           not the stride-1 kernel get SPCONV_EINVAL.
+ * lowered_words  number of int32 words of `lowered`; must equal
+ *           spconv_lowered_size for the call (SPCONV_EINVAL otherwise).
  * Both borders are limited so that one padded plane has fewer than 2^31
  * elements.
  */
@@ -204,6 +213,8 @@ typedef struct spconv_options {
     int32_t residual_pad;
     const float *residual;
     int64_t max_row_nnz;
+    const int32_t *lowered;
+    int64_t lowered_words;
 } spconv_options;
 
 /*
@@ -224,6 +235,56 @@ int spconv_forward_ex(const float *in_padded, int N, int C, int H, int W, const 
                       int stride, int pad, const float *bias, uint32_t flags, const spconv_options *opt, float *out,
                       hipStream_t stream);
 
+/*
+ * Lowered entry stream (host packing). The CSR walk of the paper's "Sparse
+ * Convolution with CSR" loop re-bases every entry's offset to the kernel's
+ * staged input tile and splits it by tap parity before use; for a fixed layer
+ * and launch plan that work is the same on every call, so it can be done once
+ * on the host. The stream holds, for each (output-channel tile, wave, row slot,
+ * input-channel chunk) of the plan, a header of four int32
+ *   {start, n_even, n_odd, k}
+ * (k = the output channel of the slot, K for an empty slot; start = index of
+ * the slot's first entry of that chunk), followed by every CSR entry once as
+ * an int32 pair (LDS index of the pixel pair the tap reads for virtual pixel 0
+ * of the chunk, the value's bits), the even-parity taps of a (slot, chunk)
+ * before its odd ones, each in CSR order; then 8 zero pairs of padding. With
+ * the plan's spconv_plan_info, entry (c, r, s) of the chunk starting at
+ * channel c0 = chunk * channels_per_chunk has LDS index t = (c - c0) *
+ * lds_channel_floats + r * lds_row_pitch + s + lds_col_shift; its parity is
+ * t's, and the stored index is t rounded down to even (the kernel reads the
+ * aligned pixel pair there). Headers are ordered by (tile, wave, slot, chunk),
+ * entries by (tile, wave, slot, chunk, parity).
+ * Its layout is a function of the plan, so it is valid only for the call
+ * arguments it was packed for.
+ */
+
+/*
+ * spconv_lowered_size - int32 words of the lowered stream for a forward call
+ * with these arguments (host only; csr's arrays are not read):
+ *   4 * tiles * 16 * channels_per_wave * chunks + 2 * (nnz + 8).
+ * Errors: those of spconv_forward_ex's argument checks (opt->lowered is not
+ * looked at); SPCONV_EINVAL for a NULL words or a plan other than the
+ * stride-1 kernel.
+ */
+int spconv_lowered_size(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride, int pad,
+                        uint32_t flags, const spconv_options *opt, int64_t *words);
+
+/*
+ * spconv_pack_lowered - write the lowered stream (host). csr's arrays are host
+ * memory here: rowptr, colidx and vals are read (offset is not), and checked
+ * to be a valid CSR of a (K, C*R*S) matrix (rowptr starts at 0, does not
+ * decrease and ends at nnz; colidx strictly increasing within a row and below
+ * C*R*S). Output channels are assigned to the waves of each channel tile as
+ * the kernel would pair them (ranked by entry count, dealt in snake order).
+ * lowered  host array of capacity int32 words; spconv_lowered_size words are
+ *          written.
+ * Errors: as spconv_lowered_size; SPCONV_EINVAL for a NULL lowered or an
+ * invalid CSR; SPCONV_ECAPACITY when capacity is below spconv_lowered_size
+ * (nothing written).
+ */
+int spconv_pack_lowered(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride, int pad,
+                        uint32_t flags, const spconv_options *opt, int32_t *lowered, int64_t capacity);
+
 /* Kernel families reported by spconv_plan. */
 #define SPCONV_KERNEL_STRIDE1 1 /* stride 1: channel-chunked LDS staging, lanes own padded-width pixels */
 #define SPCONV_KERNEL_GENERIC 2 /* any stride */
@@ -241,6 +302,13 @@ typedef struct spconv_plan_info {
     int32_t workgroups;            /* grid size */
     int32_t threads_per_workgroup;
     int64_t lds_bytes;             /* dynamic LDS per workgroup */
+    /* Stride-1 kernel (0 otherwise): where tap (r, s) of input channel c of a
+     * chunk starting at channel c0 sits in the staged tile, as an LDS float
+     * index for virtual pixel 0:  (c - c0)*lds_channel_floats + r*lds_row_pitch
+     * + s + lds_col_shift. */
+    int32_t lds_channel_floats;
+    int32_t lds_row_pitch;
+    int32_t lds_col_shift;
 } spconv_plan_info;
 
 /*

@@ -36,6 +36,7 @@
 #include <cstdint>
 #include <cstring>
 #include <type_traits>
+#include <vector>
 
 #include "common.h"
 #include "spconv.h"
@@ -436,7 +437,17 @@ struct FwdArgs {
     // one stored row or outside the output, so each pair moves with one
     // two-dword access
     int pair_store;
+    // lowered entry stream (spconv_pack_lowered): headers {start, n_even,
+    // n_odd, k} per (channel tile, wave, row slot, chunk), then n_entries
+    // (LDS index, weight) pairs and an over-read pad of kLwPad pairs
+    int lw_headers;
+    int lw_entries;
 };
+
+// Entries fetched per scalar load in the lowered walk (one s_load_dwordx16),
+// and the pad of entries after the stream that such loads may read.
+constexpr int kLwBatch = 8;
+constexpr int kLwPad = kLwBatch;
 
 // Queue asynchronous global->LDS copies of one channel chunk: for each image of
 // the group and each channel of the chunk, seg_len consecutive floats (the
@@ -776,6 +787,62 @@ __device__ __forceinline__ void run_range(float2 (&acc)[IPW][PJ], int lo, float 
     }
 }
 
+// Walk of one list of a lowered stream: n entries (LDS index of the pixel
+// pair read for virtual pixel 0 of the chunk, weight bits) from entry j on,
+// accumulated into acc. Entries arrive in batches of kLwBatch with one scalar
+// load each, so index and weight are wave-uniform SGPRs: an entry costs one
+// address add and its FMAs (the weight is the FMAs' scalar operand), no
+// broadcast. Software pipeline of NB pixel-pair buffers as in run_range; the
+// next batch is loaded NB entries before its first use, so its scalar load
+// overlaps one entry's FMAs (scalar loads complete out of order with LDS
+// reads, so the first LDS wait after it waits for both).
+template <int B>
+struct LwBatch {
+    int v[2 * B];
+};
+
+template <int NB, int PJ, int IPW>
+__device__ __forceinline__ void run_lowered(float2 (&acc)[IPW][PJ], const int32_t *__restrict__ ent, int j, int n,
+                                            const float *lds, int qv, int img_lds) {
+    if (n <= 0) return;
+    constexpr int B = kLwBatch;
+    static_assert(B % NB == 0, "buffer rotation must repeat every batch");
+    f32x2 x[NB][IPW][PJ];
+    LwBatch<B> b = *reinterpret_cast<const LwBatch<B> *>(ent + 2 * j);
+#pragma unroll
+    for (int u = 0; u < NB - 1; ++u)
+        if (u < n) load_pairs(x[u], lds, b.v[2 * u] + qv, img_lds);
+    int r = n;
+    // Full batches followed by at least one more entry: the loads of entry
+    // u + NB - 1 may come from the next batch.
+    for (; r > B; r -= B) {
+        LwBatch<B> nb;
+#pragma unroll
+        for (int u = 0; u < B; ++u) {
+            if (u == B - NB) nb = *reinterpret_cast<const LwBatch<B> *>(ent + 2 * (j + B));
+            const int f = u + NB - 1;  // entry whose loads issue now
+            if (f < B) {
+                load_pairs(x[f % NB], lds, b.v[2 * f] + qv, img_lds);
+            } else if (f - B < r - B) {
+                load_pairs(x[f % NB], lds, nb.v[2 * (f - B)] + qv, img_lds);
+            }
+            fma_pairs(acc, x[u % NB], __int_as_float(b.v[2 * u + 1]));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        b = nb;
+        j += B;
+    }
+    // Last batch: r entries (1..B); entries below NB - 1 are in flight.
+#pragma unroll
+    for (int u = 0; u < B; ++u) {
+        if (u >= r) break;
+        const int f = u + NB - 1;
+        if (f < r) load_pairs(x[f % NB], lds, b.v[2 * f] + qv, img_lds);
+        fma_pairs(acc, x[u % NB], __int_as_float(b.v[2 * u + 1]));
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // Pipeline depth of the stride-1 kernel: deeper for fewer FMAs per entry
 // (IPW * PI), where the 128 VGPRs of four waves per SIMD hold the buffers
 // (accumulators plus buffers within 98 floats, at most two channels a wave:
@@ -827,17 +894,28 @@ __device__ __forceinline__ void set_progress_prio(int done, int total) {
         __builtin_amdgcn_s_setprio(3);
 }
 
-template <int PI, int IPW, int RPW, bool POOL>
+// Pipeline depth of the lowered walk: a divisor of its batch, four buffers for
+// tilings with few FMAs per entry where the registers hold them.
+template <int PI, int IPW, int RPW>
+constexpr int lowered_pipeline_buffers() {
+    return (IPW * PI <= 8 && 2 * RPW * IPW * PI + 4 * IPW * PI <= 80) ? 4 : 2;
+}
+
+// LW: the CSR rows come as a lowered entry stream (lw, see FwdArgs) instead of
+// rowptr/offset/vals: rows are assigned to waves by the stream's headers and
+// each (row, chunk) is two ready lists of (LDS index, weight) per tap parity.
+template <int PI, int IPW, int RPW, bool POOL, bool LW>
 __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4))) void spconv_s1_kernel(
     FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ offset,
-    const float *__restrict__ vals, const float *__restrict__ bias, const float *__restrict__ res,
-    float *__restrict__ out) {
+    const float *__restrict__ vals, const int32_t *__restrict__ lw, const float *__restrict__ bias,
+    const float *__restrict__ res, float *__restrict__ out) {
     extern __shared__ float lds[];
     constexpr int KT = RPW * kS1Waves;  // output channels per workgroup
     constexpr int PJ = PI / 2;          // pixel pairs per lane per image
     static_assert(PI % 2 == 0, "pixels per lane come in pairs");
     constexpr int NB = pipeline_buffers<PI, IPW, RPW>();
     constexpr bool kCompact = NB > 2;  // compacted windows where entries have few FMAs
+    constexpr int NBL = lowered_pipeline_buffers<PI, IPW, RPW>();
 
     const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
@@ -854,7 +932,21 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
     // w, 2*16-1-w, 2*16+w, ...), so heavy and light channels share a wave and
     // the waves' loads even out.
     int krow[RPW];
-    if constexpr (RPW == 1) {
+    // Lowered stream: the header of (row slot i, chunk ch) of this wave, and
+    // the entries after all headers.
+    const int32_t *lw_ent = LW ? lw + 4 * (size_t)a.lw_headers : nullptr;
+    const int hslot = (kt * kS1Waves + wave) * RPW;
+    auto lw_header = [&](int i, int ch) {
+        return *reinterpret_cast<const int4 *>(lw + 4 * (size_t)((hslot + i) * a.nchunks + ch));
+    };
+    int4 lwh[RPW];
+    if constexpr (LW) {
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            lwh[i] = lw_header(i, 0);
+            krow[i] = lwh[i].w;
+        }
+    } else if constexpr (RPW == 1) {
         krow[0] = kt * KT + wave;
     } else {
         const int k0 = kt * KT;
@@ -876,8 +968,8 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
         const int k = krow[i];
-        cur[i] = (k < a.K) ? rowptr[k] : 0;
-        end[i] = (k < a.K) ? rowptr[k + 1] : 0;
+        cur[i] = (!LW && k < a.K) ? rowptr[k] : 0;
+        end[i] = (!LW && k < a.K) ? rowptr[k + 1] : 0;
     }
 
     // accE: pixels (2l + 128j, 2l+1 + 128j) from even taps; accO: pixels
@@ -908,16 +1000,51 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
         __syncthreads();
     }
     stage_chunk_s1(a, xp, lds, 0, ig, y0, wave, lane);
+    if constexpr (!LW) {
 #pragma unroll
-    for (int i = 0; i < RPW; ++i) {
-        next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
-        win[i] = decode_window<kCompact>(a, next[i], end[i], bound_of(0), vb_of(0), lane);
+        for (int i = 0; i < RPW; ++i) {
+            next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
+            win[i] = decode_window<kCompact>(a, next[i], end[i], bound_of(0), vb_of(0), lane);
+        }
     }
     wait_async_copies();
     __syncthreads();
 
     for (int ch = 0; ch < a.nchunks; ++ch) {
         const bool more = ch + 1 < a.nchunks;
+        if constexpr (LW) {
+            if (more) stage_chunk_s1(a, xp, lds + ((ch + 1) & 1) * a.buf_floats, ch + 1, ig, y0, wave, lane);
+            // Entry lists of this chunk, clamped to the stream.
+            int st[RPW], ne[RPW], no[RPW];
+            int total = 0, done = 0;
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) {
+                st[i] = min(max(lwh[i].x, 0), a.lw_entries);
+                ne[i] = min(max(lwh[i].y, 0), a.lw_entries - st[i]);
+                no[i] = min(max(lwh[i].z, 0), a.lw_entries - st[i] - ne[i]);
+                total += ne[i] + no[i];
+            }
+            const int qv = (ch & 1) * a.buf_floats + q;
+            set_progress_prio(0, total);
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) {
+                run_lowered<NBL>(accE[i], lw_ent, st[i], ne[i], lds, qv, a.img_lds);
+                done += ne[i];
+                set_progress_prio(done, total);
+                run_lowered<NBL>(accO[i], lw_ent, st[i] + ne[i], no[i], lds, qv, a.img_lds);
+                done += no[i];
+                set_progress_prio(done, total);
+            }
+            if (more) {
+#pragma unroll
+                for (int i = 0; i < RPW; ++i) lwh[i] = lw_header(i, ch + 1);
+            }
+            if (POOL || more) {
+                wait_async_copies();
+                __syncthreads();
+            }
+            continue;
+        }
         if (more) {
             stage_chunk_s1(a, xp, lds + ((ch + 1) & 1) * a.buf_floats, ch + 1, ig, y0, wave, lane);
             // Fetch the next chunk's windows now, from where this chunk's
@@ -1127,6 +1254,7 @@ __global__ __launch_bounds__(kThreads) void spconv_generic_kernel(FwdArgs a, con
                                                                   const int32_t *__restrict__ rowptr,
                                                                   const int32_t *__restrict__ offset,
                                                                   const float *__restrict__ vals,
+                                                                  const int32_t *__restrict__ lw,
                                                                   const float *__restrict__ bias,
                                                                   const float *__restrict__ res,
                                                                   float *__restrict__ out) {
@@ -1312,8 +1440,8 @@ struct Plan {
     size_t lds_bytes = 0;
 };
 
-using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_t *, const float *, const float *,
-                          const float *, float *);
+using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_t *, const float *, const int32_t *,
+                          const float *, const float *, float *);
 
 // Stride-1 kernel instances: (PI, IPW, RPW, pools), pools bit 0 = built
 // without the pool epilogue, bit 1 = with it. Four waves per SIMD leave 128
@@ -1343,7 +1471,7 @@ constexpr S1Variant kS1Variants[] = {
 constexpr int kNumS1Variants = (int)(sizeof(kS1Variants) / sizeof(kS1Variants[0]));
 
 template <int I>
-FwdKernel pick_s1_from(int PI, int IPW, int RPW, bool pool) {
+FwdKernel pick_s1_from(int PI, int IPW, int RPW, bool pool, bool lowered) {
     if constexpr (I == kNumS1Variants) {
         return nullptr;
     } else {
@@ -1352,13 +1480,17 @@ FwdKernel pick_s1_from(int PI, int IPW, int RPW, bool pool) {
                       "tiling exceeds the register budget");
         if (v.pi == PI && v.ipw == IPW && v.rpw == RPW) {
             if (pool) {
-                if constexpr ((v.pools & 2) != 0) return spconv_s1_kernel<v.pi, v.ipw, v.rpw, true>;
+                if constexpr ((v.pools & 2) != 0)
+                    return lowered ? spconv_s1_kernel<v.pi, v.ipw, v.rpw, true, true>
+                                   : spconv_s1_kernel<v.pi, v.ipw, v.rpw, true, false>;
                 return nullptr;
             }
-            if constexpr ((v.pools & 1) != 0) return spconv_s1_kernel<v.pi, v.ipw, v.rpw, false>;
+            if constexpr ((v.pools & 1) != 0)
+                return lowered ? spconv_s1_kernel<v.pi, v.ipw, v.rpw, false, true>
+                               : spconv_s1_kernel<v.pi, v.ipw, v.rpw, false, false>;
             return nullptr;
         }
-        return pick_s1_from<I + 1>(PI, IPW, RPW, pool);
+        return pick_s1_from<I + 1>(PI, IPW, RPW, pool, lowered);
     }
 }
 
@@ -1367,7 +1499,9 @@ FwdKernel pick_s1_from(int PI, int IPW, int RPW, bool pool) {
 constexpr int kPiSingle[] = {24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4};
 constexpr int kPiMulti[] = {8, 6, 4, 2};
 
-FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool) { return pick_s1_from<0>(PI, IPW, RPW, pool); }
+FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool, bool lowered = false) {
+    return pick_s1_from<0>(PI, IPW, RPW, pool, lowered);
+}
 
 // Picks the stride-1 tiling with the smallest modelled run time. The model
 // counts LDS cycles: every nonzero costs a wave IPW*PI LDS reads (2 cycles
@@ -1545,10 +1679,10 @@ bool plan_generic(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int strid
     return true;
 }
 
-FwdKernel pick_kernel(const Plan &pl, bool pool) {
+FwdKernel pick_kernel(const Plan &pl, bool pool, bool lowered = false) {
     if (pl.kind == Kind::kGeneric)
-        return pool ? spconv_generic_kernel<4, 4, true> : spconv_generic_kernel<4, 4, false>;
-    return pick_s1(pl.PI, pl.IPW, pl.RPW, pool);
+        return lowered ? nullptr : (pool ? spconv_generic_kernel<4, 4, true> : spconv_generic_kernel<4, 4, false>);
+    return pick_s1(pl.PI, pl.IPW, pl.RPW, pool, lowered);
 }
 
 bool out_extent(int in, int f, int stride, int pad, int *o) {
@@ -1746,6 +1880,7 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.lds_shift = row16 ? (4 - pad % 4) % 4 : 0;
     a.dma16 = row16 ? 1 : 0;
     a.pair_store = 0;
+    a.lw_headers = a.lw_entries = 0;
     if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift)) return SPCONV_EINVAL;
     if (!div_magic((uint32_t)a.vp, &a.vp_magic, &a.vp_shift)) return SPCONV_EINVAL;
     a.H = H;
@@ -1802,6 +1937,14 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
 
 // Border and residual options of spconv_forward_ex, checked and folded into
 // the args.
+// Lowered stream of a stride-1 plan: headers (4 words each) per (channel
+// tile, wave, row slot, chunk), then nnz entries and kLwPad pad entries (2
+// words each).
+int lowered_headers(const Plan &pl) { return pl.nktiles * kS1Waves * pl.RPW * pl.nchunks; }
+long long lowered_words(const Plan &pl, long long nnz) {
+    return 4LL * lowered_headers(pl) + 2LL * (nnz + kLwPad);
+}
+
 int apply_epilogue(const spconv_options *opt, FwdArgs *a) {
     if (!opt) return SPCONV_OK;
     if (opt->out_pad < 0 || (opt->residual && opt->residual_pad < 0)) return SPCONV_EINVAL;
@@ -1840,7 +1983,15 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
     a.pair_store = pl.kind == Kind::kStride1 && (flags & SPCONV_MAXPOOL2X2) == 0 && a.vp % 2 == 0 &&
                    a.Wo % 2 == 0 && (reinterpret_cast<uintptr_t>(out) & 3) == 0 &&
                    (!residual || (reinterpret_cast<uintptr_t>(residual) & 3) == 0);
-    FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0);
+    const int32_t *lowered = opt ? opt->lowered : nullptr;
+    if (lowered) {
+        if (pl.kind != Kind::kStride1 || (reinterpret_cast<uintptr_t>(lowered) & 15) != 0) return SPCONV_EINVAL;
+        if (opt->lowered_words != lowered_words(pl, csr->nnz)) return SPCONV_EINVAL;
+        a.lw_headers = lowered_headers(pl);
+        a.lw_entries = (int)csr->nnz;
+    }
+    FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0, lowered != nullptr);
+    if (!kern) return SPCONV_EINVAL;
     const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
     // Each kernel instance's dynamic-LDS limit is raised once, to the most any
     // plan of its family uses, so that launches of different shapes from
@@ -1848,7 +1999,7 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
     if (!raise_lds_limit((const void *)kern, pl.kind == Kind::kStride1 ? kS1LdsFloats * 4 : kGenericLdsBytes))
         return SPCONV_EHIP;
     hipLaunchKernelGGL(kern, dim3((unsigned)pl.total_wgs), dim3(threads), pl.lds_bytes, stream, a, in_padded,
-                       csr->rowptr, csr->offset, csr->vals, bias, residual, out);
+                       csr->rowptr, csr->offset, csr->vals, lowered, bias, residual, out);
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 
@@ -1879,6 +2030,9 @@ extern "C" int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, in
     info->workgroups = pl.total_wgs;
     info->threads_per_workgroup = (int32_t)(s1 ? kS1Threads : kThreads);
     info->lds_bytes = (int64_t)pl.lds_bytes;
+    info->lds_channel_floats = s1 ? pl.PLp : 0;
+    info->lds_row_pitch = s1 ? a.vp : 0;
+    info->lds_col_shift = s1 ? a.lds_shift : 0;
     return SPCONV_OK;
 }
 
@@ -1905,5 +2059,93 @@ extern "C" int spconv_kernel_variants(int32_t kernel, int32_t *variants, int32_t
                 if (v.pools & (1 << pool)) put(v.pi, v.ipw, v.rpw, pool);
     }
     *count = n;
+    return SPCONV_OK;
+}
+
+extern "C" int spconv_lowered_size(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride,
+                                   int pad, uint32_t flags, const spconv_options *opt, int64_t *words) {
+    if (!words) return SPCONV_EINVAL;
+    Plan pl;
+    FwdArgs a;
+    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, &pl, &a);
+    if (rc != SPCONV_OK) return rc;
+    rc = apply_epilogue(opt, &a);
+    if (rc != SPCONV_OK) return rc;
+    if (pl.kind != Kind::kStride1) return SPCONV_EINVAL;
+    const long long w = lowered_words(pl, csr->nnz);
+    if (w >= (1LL << 31)) return SPCONV_EINVAL;
+    *words = w;
+    return SPCONV_OK;
+}
+
+extern "C" int spconv_pack_lowered(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride,
+                                   int pad, uint32_t flags, const spconv_options *opt, int32_t *lowered,
+                                   int64_t capacity) {
+    if (!lowered) return SPCONV_EINVAL;
+    int64_t words = 0;
+    int rc = spconv_lowered_size(N, C, H, W, csr, K, R, S, stride, pad, flags, opt, &words);
+    if (rc != SPCONV_OK) return rc;
+    Plan pl;
+    FwdArgs a;
+    rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, &pl, &a);
+    if (rc != SPCONV_OK) return rc;
+    // The CSR, read on the host: a valid (K, C*R*S) matrix.
+    const long long nnz = csr->nnz, cols = (long long)C * R * S;
+    const int32_t *rp = csr->rowptr, *ci = csr->colidx;
+    const float *va = csr->vals;
+    if (!rp || (nnz > 0 && (!ci || !va)) || rp[0] != 0 || rp[K] != nnz) return SPCONV_EINVAL;
+    for (int k = 0; k < K; ++k) {
+        if (rp[k + 1] < rp[k]) return SPCONV_EINVAL;
+        for (int j = rp[k]; j < rp[k + 1]; ++j)
+            if (ci[j] < 0 || ci[j] >= cols || (j > rp[k] && ci[j] <= ci[j - 1])) return SPCONV_EINVAL;
+    }
+    if (capacity < words) return SPCONV_ECAPACITY;
+    const int KT = kS1Waves * pl.RPW;
+    const int nh = lowered_headers(pl);
+    int32_t *hdr = lowered;
+    int32_t *ent = lowered + 4LL * nh;
+    long long e = 0;  // entries written
+    std::vector<int> slot_row(KT);
+    std::vector<int> order(KT);
+    for (int kt = 0; kt < pl.nktiles; ++kt) {
+        const int k0 = kt * KT;
+        // Rows of this channel tile by entry count, most first (ties: lower
+        // channel first), dealt to (slot i, wave w) in snake order: ranks
+        // i*16 + w for even i, i*16 + 15 - w for odd i. One row per wave
+        // needs no ranking.
+        for (int j = 0; j < KT; ++j) order[j] = j;
+        auto nz = [&](int j) { return k0 + j < K ? rp[k0 + j + 1] - rp[k0 + j] : -1; };
+        if (pl.RPW > 1)
+            std::stable_sort(order.begin(), order.end(), [&](int x, int y) { return nz(x) > nz(y); });
+        for (int r = 0; r < KT; ++r) {
+            const int i = r / kS1Waves, w = (i & 1) ? kS1Waves - 1 - r % kS1Waves : r % kS1Waves;
+            slot_row[w * pl.RPW + i] = k0 + order[r];
+        }
+        for (int w = 0; w < kS1Waves; ++w)
+            for (int i = 0; i < pl.RPW; ++i) {
+                const int k = slot_row[w * pl.RPW + i];
+                for (int ch = 0; ch < pl.nchunks; ++ch) {
+                    int32_t *h = hdr + 4LL * (((long long)(kt * kS1Waves + w) * pl.RPW + i) * pl.nchunks + ch);
+                    h[0] = (int32_t)e;
+                    h[1] = h[2] = 0;
+                    h[3] = k < K ? k : K;
+                    if (k >= K) continue;
+                    const int c0 = ch * pl.Cc, c1 = std::min(C, c0 + pl.Cc);
+                    for (int parity = 0; parity < 2; ++parity)
+                        for (int j = rp[k]; j < rp[k + 1]; ++j) {
+                            const int c = ci[j] / (R * S), t = ci[j] % (R * S);
+                            if (c < c0 || c >= c1) continue;
+                            const int idx = (c - c0) * pl.PLp + (t / S) * a.vp + (t % S) + a.lds_shift;
+                            if ((idx & 1) != parity) continue;
+                            ent[2 * e] = idx - parity;
+                            std::memcpy(&ent[2 * e + 1], &va[j], sizeof(float));
+                            ++e;
+                            ++h[1 + parity];
+                        }
+                }
+            }
+    }
+    if (e != nnz) return SPCONV_EINVAL;  // every entry lies in one chunk of one slot
+    std::memset(ent + 2 * e, 0, sizeof(int32_t) * 2 * kLwPad);
     return SPCONV_OK;
 }

@@ -27,7 +27,8 @@ SPCONV_UNPADDED_INPUT = 4
 
 EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "spconv_forward", "spconv_forward_ex", "spconv_plan",
             "spconv_output_shape", "spconv_strerror", "spconv_dense_size", "spconv_pack_dense",
-            "spconv_forward_dense", "spconv_dense_plan", "spconv_select_path", "spconv_kernel_variants")
+            "spconv_forward_dense", "spconv_dense_plan", "spconv_select_path", "spconv_kernel_variants",
+            "spconv_lowered_size", "spconv_pack_lowered")
 SPCONV_KERNEL_STRIDE1 = 1
 SPCONV_KERNEL_GENERIC = 2
 SPCONV_KERNEL_DENSE = 3
@@ -46,7 +47,7 @@ class spconv_csr(ctypes.Structure):
 class spconv_options(ctypes.Structure):
     """Mirror of ``struct spconv_options``."""
     _fields_ = [("out_pad", ctypes.c_int32), ("residual_pad", ctypes.c_int32), ("residual", ctypes.c_void_p),
-                ("max_row_nnz", ctypes.c_int64)]
+                ("max_row_nnz", ctypes.c_int64), ("lowered", ctypes.c_void_p), ("lowered_words", ctypes.c_int64)]
 
 
 class spconv_plan_info(ctypes.Structure):
@@ -55,7 +56,8 @@ class spconv_plan_info(ctypes.Structure):
                 ("channels_per_wave", ctypes.c_int32), ("tile_rows", ctypes.c_int32),
                 ("tiles_per_image", ctypes.c_int32), ("channels_per_chunk", ctypes.c_int32),
                 ("chunks", ctypes.c_int32), ("workgroups", ctypes.c_int32), ("threads_per_workgroup", ctypes.c_int32),
-                ("lds_bytes", ctypes.c_int64)]
+                ("lds_bytes", ctypes.c_int64), ("lds_channel_floats", ctypes.c_int32), ("lds_row_pitch", ctypes.c_int32),
+                ("lds_col_shift", ctypes.c_int32)]
 
 
 _c_int = ctypes.c_int
@@ -98,6 +100,12 @@ def _bind(lib):
     lib.spconv_dense_plan.argtypes = [_c_int] * 8 + [ctypes.c_uint32, ctypes.POINTER(spconv_plan_info)]
     lib.spconv_select_path.restype = _c_int
     lib.spconv_select_path.argtypes = [_c_int] * 9 + [ctypes.c_int64, ctypes.c_uint32, ctypes.POINTER(_c_int)]
+    lib.spconv_lowered_size.restype = _c_int
+    lib.spconv_lowered_size.argtypes = [_c_int] * 4 + [ctypes.POINTER(spconv_csr)] + [_c_int] * 5 + [
+        ctypes.c_uint32, ctypes.POINTER(spconv_options), ctypes.POINTER(ctypes.c_int64)]
+    lib.spconv_pack_lowered.restype = _c_int
+    lib.spconv_pack_lowered.argtypes = [_c_int] * 4 + [ctypes.POINTER(spconv_csr)] + [_c_int] * 5 + [
+        ctypes.c_uint32, ctypes.POINTER(spconv_options), _vp, ctypes.c_int64]
     lib.spconv_kernel_variants.restype = _c_int
     lib.spconv_kernel_variants.argtypes = [ctypes.c_int32, _vp, ctypes.c_int32, ctypes.POINTER(ctypes.c_int32)]
     return lib
@@ -173,6 +181,28 @@ def spconv_pack_csr(w: np.ndarray, mask: np.ndarray | None, Hp: int, Wp: int) ->
     _check(_lib.spconv_pack_csr(_np_ptr(w), _np_ptr(m), K, C, R, S, Hp, Wp, _np_ptr(rowptr), _np_ptr(colidx),
                                 _np_ptr(offset), _np_ptr(vals), n, ctypes.byref(nnz)), "spconv_pack_csr")
     return HostCSR(K, C, R, S, Hp, Wp, rowptr, colidx[:n], offset[:n], vals[:n])
+
+
+def host_csr_struct(host: HostCSR) -> spconv_csr:
+    """A ``spconv_csr`` whose arrays are the host arrays of ``host`` (for the
+    host-side calls: spconv_pack_lowered, and plans)."""
+    return spconv_csr(host.K, host.C, host.R, host.S, host.Hp, host.Wp, host.nnz, host.rowptr.ctypes.data,
+                      host.colidx.ctypes.data, host.offset.ctypes.data, host.vals.ctypes.data)
+
+
+def spconv_pack_lowered(host: HostCSR, N: int, H: int, W: int, stride: int, pad: int, flags: int,
+                        max_row_nnz: int = 0) -> np.ndarray:
+    """The lowered entry stream (int32 host array) for a forward call with these
+    arguments (see ``spconv_pack_lowered`` in include/spconv.h)."""
+    st = host_csr_struct(host)
+    opt = spconv_options(0, 0, None, max_row_nnz, None, 0)
+    words = ctypes.c_int64()
+    _check(_lib.spconv_lowered_size(N, host.C, H, W, ctypes.byref(st), host.K, host.R, host.S, stride, pad, flags,
+                                    ctypes.byref(opt), ctypes.byref(words)), "spconv_lowered_size")
+    out = np.empty(words.value, np.int32)
+    _check(_lib.spconv_pack_lowered(N, host.C, H, W, ctypes.byref(st), host.K, host.R, host.S, stride, pad, flags,
+                                    ctypes.byref(opt), out.ctypes.data, out.size), "spconv_pack_lowered")
+    return out
 
 
 def spconv_dense_size(K: int, C: int, R: int, S: int) -> int:
@@ -327,12 +357,14 @@ def spconv_forward(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R
 
 def spconv_forward_ex(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int, R: int, S: int, stride: int,
                       pad: int, bias=None, flags: int = SPCONV_RELU, out_pad: int = 0, residual=None,
-                      residual_pad: int = 0, out=None, stream=None, max_row_nnz: int | None = None):
+                      residual_pad: int = 0, out=None, stream=None, max_row_nnz: int | None = None, lowered=None):
     """``spconv_forward`` with options: the stored planes get a zero border of
     ``out_pad`` (the next layer's padded input), ``residual`` (on the
     convolution's grid, with a border of ``residual_pad``) is added before the
-    activation, and the planner gets ``max_row_nnz`` (default: the value
-    measured on ``csr``'s host arrays; 0 = unknown)."""
+    activation, the planner gets ``max_row_nnz`` (default: the value measured
+    on ``csr``'s host arrays; 0 = unknown), and ``lowered`` (a device int32
+    tensor from ``spconv_pack_lowered`` for this call) feeds the stride-1
+    kernel its entries ready-made."""
     Hs, Ws = spconv_output_shape(H, W, R, S, stride, pad, flags)
     s = _stream_of(stream, xp.device)
     if out is None:
@@ -343,7 +375,15 @@ def spconv_forward_ex(xp, N: int, C: int, H: int, W: int, csr: DeviceCSR, K: int
     _check_numel(bias, K, "bias")
     _check_numel(residual, N * K * (Hc + 2 * residual_pad) * (Wc + 2 * residual_pad), "residual")
     hint = csr.max_row_nnz if max_row_nnz is None else max_row_nnz
-    opt = spconv_options(out_pad, residual_pad, _dev_ptr(residual, "residual"), hint)
+    lw = None
+    if lowered is not None:
+        import torch
+        if not isinstance(lowered, torch.Tensor) or lowered.device.type != "cuda" or lowered.dtype != torch.int32 \
+                or not lowered.is_contiguous():
+            raise TypeError("lowered must be a contiguous int32 device tensor")
+        lw = lowered.data_ptr()
+    opt = spconv_options(out_pad, residual_pad, _dev_ptr(residual, "residual"), hint, lw,
+                         0 if lowered is None else lowered.numel())
     _check(_lib.spconv_forward_ex(_dev_ptr(xp, "xp"), N, C, H, W, ctypes.byref(csr.struct), K, R, S, stride, pad,
                                   _dev_ptr(bias, "bias"), flags, ctypes.byref(opt), _dev_ptr(out, "out"),
                                   s.cuda_stream), "spconv_forward_ex")
@@ -365,7 +405,7 @@ def spconv_forward_dense(xp, N: int, C: int, H: int, W: int, packed, K: int, R: 
     _check_numel(out, N * K * (Hs + 2 * out_pad) * (Ws + 2 * out_pad), "out")
     _check_numel(bias, K, "bias")
     _check_numel(residual, N * K * (Hc + 2 * residual_pad) * (Wc + 2 * residual_pad), "residual")
-    opt = spconv_options(out_pad, residual_pad, _dev_ptr(residual, "residual"), 0)
+    opt = spconv_options(out_pad, residual_pad, _dev_ptr(residual, "residual"), 0, None, 0)
     _check(_lib.spconv_forward_dense(_dev_ptr(xp, "xp"), N, C, H, W, _dev_ptr(packed, "packed"), K, R, S, pad,
                                      _dev_ptr(bias, "bias"), flags, ctypes.byref(opt), _dev_ptr(out, "out"),
                                      s.cuda_stream), "spconv_forward_dense")
@@ -381,7 +421,7 @@ def spconv_plan(N: int, C: int, H: int, W: int, csr, K: int, R: int, S: int, str
     struct = csr.struct if isinstance(csr, DeviceCSR) else csr
     if max_row_nnz is None:
         max_row_nnz = csr.max_row_nnz if isinstance(csr, DeviceCSR) else 0
-    opt = spconv_options(0, 0, None, max_row_nnz)
+    opt = spconv_options(0, 0, None, max_row_nnz, None, 0)
     info = spconv_plan_info()
     _check(_lib.spconv_plan(N, C, H, W, ctypes.byref(struct), K, R, S, stride, pad, flags, ctypes.byref(opt),
                             ctypes.byref(info)), "spconv_plan")
@@ -415,8 +455,14 @@ class SparseConvLayer:
 
     def __init__(self, w: np.ndarray, mask: np.ndarray | None, bias: np.ndarray | None, H: int, W: int,
                  stride: int = 1, pad: int = 1, relu: bool = True, pool: bool = False, device="cuda",
-                 path: str = "sparse", N: int | None = None):
+                 path: str = "sparse", N: int | None = None, lowered: bool = True):
         import torch
+        # lowered: feed stride-1 sparse plans their entries as a lowered stream
+        # (spconv_pack_lowered, packed once per batch size and flags); False
+        # keeps the plain CSR walk.
+        self.use_lowered = lowered
+        self.device = device
+        self._lowered_cache = {}
         self.K, self.C, self.R, self.S = (int(v) for v in w.shape)
         self.H, self.W, self.stride, self.pad = H, W, stride, pad
         self.flags = flags_of(relu, pool)
@@ -460,7 +506,26 @@ class SparseConvLayer:
         # skew (max_row_nnz) whatever the epilogue.
         return spconv_forward_ex(xp, N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride,
                                  self.pad, self.bias, flags, out_pad=out_pad, residual=residual,
-                                 residual_pad=residual_pad, out=out, stream=stream)
+                                 residual_pad=residual_pad, out=out, stream=stream, lowered=self.lowered(N, flags))
+
+    def lowered(self, N: int, flags: int | None = None):
+        """The device lowered entry stream for batch size ``N`` and ``flags``
+        (cached), or None when this layer does not use one (dense path, an
+        any-stride plan, or ``lowered=False``)."""
+        flags = self.flags if flags is None else flags
+        if self.path != "sparse" or not self.use_lowered:
+            return None
+        key = (N, flags)
+        if key not in self._lowered_cache:
+            import torch
+            p = spconv_plan(N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride, self.pad, flags)
+            t = None
+            if p["kernel"] == SPCONV_KERNEL_STRIDE1:
+                host = spconv_pack_lowered(self.host_csr, N, self.H, self.W, self.stride, self.pad, flags,
+                                           self.csr.max_row_nnz)
+                t = torch.from_numpy(host).to(self.device)
+            self._lowered_cache[key] = t
+        return self._lowered_cache[key]
 
     # The kernels stage an unpadded input one image row per LDS-DMA instruction,
     # and on MI355X such a copy costs about the same per instruction up to 1

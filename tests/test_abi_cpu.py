@@ -36,7 +36,7 @@ def test_header_declares_the_boundary():
     assert declared_functions() == sorted(
         ["spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "spconv_forward", "spconv_forward_ex",
          "spconv_plan", "spconv_dense_size", "spconv_pack_dense", "spconv_forward_dense", "spconv_dense_plan",
-         "spconv_select_path", "spconv_kernel_variants",
+         "spconv_select_path", "spconv_kernel_variants", "spconv_lowered_size", "spconv_pack_lowered",
          "spconv_output_shape", "spconv_strerror"])
 
 

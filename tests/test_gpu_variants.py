@@ -40,18 +40,30 @@ def check_close(gpu, ref, ab, what):
 
 @pytest.mark.parametrize("case", vc.CASES, ids=[f"{c[0]}{c[1]}" for c in vc.CASES])
 def test_instance_against_oracle(sp, case):
+    """Each instance against the oracle; stride-1 instances in both forms (the
+    plain CSR walk and the lowered entry stream), which must agree bit for
+    bit (same entries, same summation order)."""
     import torch
     kind, variant, N, C, K, H, W, d, skew, pool, seed = case
     layer = vc.case_layer(case)
     R, S = layer.w.shape[2], layer.w.shape[3]
     print("[case]", kind, variant, (N, C, K, H, W, R, S), "density", d, "skew", skew, flush=True)
-    L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, 1, layer.pad, True, pool,
-                           path="dense" if kind == "dense" else "sparse")
-    plan = L.plan(N)
-    got = (R, S, plan["pixels_per_lane"], int(pool)) if kind == "dense" else \
-        (plan["pixels_per_lane"], plan["images_per_group"], plan["channels_per_wave"], int(pool))
-    assert got == variant, (got, plan)
-    out = L.run(torch.from_numpy(layer.x).cuda())
-    torch.cuda.synchronize()
-    ref, ab = oracle.conv(layer.x, layer.w, layer.mask, layer.bias, 1, layer.pad, True, pool)
-    check_close(out.cpu().numpy(), ref, ab, f"{kind} {variant}")
+    outs = {}
+    ref = ab = None
+    for lowered in ((False, True) if kind == "s1" else (False,)):
+        L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, 1, layer.pad, True, pool,
+                               path="dense" if kind == "dense" else "sparse", lowered=lowered)
+        plan = L.plan(N)
+        got = (R, S, plan["pixels_per_lane"], int(pool)) if kind == "dense" else \
+            (plan["pixels_per_lane"], plan["images_per_group"], plan["channels_per_wave"], int(pool))
+        assert got == variant, (got, plan)
+        assert (L.lowered(N) is not None) == lowered
+        print("[case]   lowered" if lowered else "[case]   plain", flush=True)
+        out = L.run(torch.from_numpy(layer.x).cuda())
+        torch.cuda.synchronize()
+        outs[lowered] = out.cpu().numpy()
+        if ref is None:
+            ref, ab = oracle.conv(layer.x, layer.w, layer.mask, layer.bias, 1, layer.pad, True, pool)
+        check_close(outs[lowered], ref, ab, f"{kind} {variant} lowered={lowered}")
+    if len(outs) == 2:
+        assert np.array_equal(outs[False].view(np.uint32), outs[True].view(np.uint32))

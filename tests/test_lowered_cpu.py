@@ -1,0 +1,181 @@
+"""Host-side checks of the lowered entry stream (no GPU needed).
+
+``spconv_pack_lowered`` is compared word for word with an independent numpy
+construction of the layout include/spconv.h documents (headers per (tile, wave,
+slot, chunk), rows ranked by entry count and dealt in snake order, entries
+re-based to the plan's staged tile and split by tap parity), over layers whose
+plans cover one, two and four rows per wave, one and several chunks, several
+images per tile, pooling and the unpadded-input tile geometry; its errors and
+the forward call's checks of a stream are exercised with never-dereferenced
+addresses.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+from paper_2005_04091_amd import synth
+
+
+@pytest.fixture(scope="module")
+def sp():
+    from paper_2005_04091_amd import spconv
+    return spconv
+
+
+def reference_stream(host, plan, K, C, R, S):
+    """The documented layout, built directly from the CSR arrays."""
+    rpw, cc, nch = plan["channels_per_wave"], plan["channels_per_chunk"], plan["chunks"]
+    plp, vp, shift = plan["lds_channel_floats"], plan["lds_row_pitch"], plan["lds_col_shift"]
+    kt_rows = 16 * rpw
+    nkt = -(-K // kt_rows)
+    rp, ci, va = host.rowptr, host.colidx, host.vals.view(np.int32)
+    headers, entries = [], []
+    for kt in range(nkt):
+        k0 = kt * kt_rows
+        nz = [int(rp[k0 + j + 1] - rp[k0 + j]) if k0 + j < K else -1 for j in range(kt_rows)]
+        order = sorted(range(kt_rows), key=lambda j: (-nz[j], j)) if rpw > 1 else list(range(kt_rows))
+        slot = {}
+        for rank, j in enumerate(order):
+            i, w = divmod(rank, 16)
+            slot[(15 - w if i % 2 else w, i)] = k0 + j
+        for w in range(16):
+            for i in range(rpw):
+                k = slot[(w, i)]
+                for ch in range(nch):
+                    start, counts = len(entries), [0, 0]
+                    if k < K:
+                        for parity in (0, 1):
+                            for j in range(rp[k], rp[k + 1]):
+                                c, t = divmod(int(ci[j]), R * S)
+                                r, s = divmod(t, S)
+                                if not ch * cc <= c < min(C, (ch + 1) * cc):
+                                    continue
+                                idx = (c - ch * cc) * plp + r * vp + s + shift
+                                if idx % 2 != parity:
+                                    continue
+                                entries.append((idx - parity, int(va[j])))
+                                counts[parity] += 1
+                    headers.append((start, counts[0], counts[1], min(k, K)))
+    out = np.array(headers, np.int32).reshape(-1)
+    ent = np.array(entries + [(0, 0)] * 8, np.int32).reshape(-1)
+    return np.concatenate([out, ent])
+
+
+CASES = [
+    # seed, N, C, K, H, W, pool, density, skew, unpadded
+    (1, 2, 16, 40, 20, 20, False, 0.3, False, False),
+    (2, 4, 64, 70, 30, 30, True, 0.2, True, False),
+    (3, 2, 200, 33, 12, 12, False, 0.1, True, False),    # several chunks
+    (4, 16, 3, 520, 12, 12, False, 0.3, True, False),    # four rows per wave
+    (5, 8, 3, 520, 2, 2, False, 0.05, False, False),     # several images per tile
+    (9, 32, 3, 1040, 2, 2, False, 0.05, False, False),   # four images, four rows per wave
+    (6, 2, 24, 20, 16, 16, False, 0.3, False, True),     # unpadded input, rows of 16-byte groups
+    (7, 1, 64, 64, 224, 224, False, 0.2, False, True),   # VGG-shaped, unpadded
+    (8, 3, 5, 7, 9, 13, True, 0.5, False, False),        # odd widths
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"c{c[0]}" for c in CASES])
+def test_stream_matches_documented_layout(sp, case):
+    seed, N, C, K, H, W, pool, d, skew, unpadded = case
+    layer = synth.random_layer(7000 + seed, N, C, K, H, W, density=d, pool=pool, skew=skew)
+    host = sp.spconv_pack_csr(layer.w, layer.mask, H + 2, W + 2)
+    flags = sp.flags_of(True, pool) | (sp.SPCONV_UNPADDED_INPUT if unpadded else 0)
+    mx = int(np.diff(host.rowptr).max())
+    plan = sp.spconv_plan(N, C, H, W, sp.host_csr_struct(host), K, 3, 3, 1, 1, flags, max_row_nnz=mx)
+    assert plan["kernel"] == sp.SPCONV_KERNEL_STRIDE1
+    got = sp.spconv_pack_lowered(host, N, H, W, 1, 1, flags, mx)
+    ref = reference_stream(host, plan, K, C, 3, 3)
+    assert got.shape == ref.shape
+    assert np.array_equal(got, ref)
+    nh = -(-K // (16 * plan["channels_per_wave"])) * 16 * plan["channels_per_wave"] * plan["chunks"]
+    assert got.size == 4 * nh + 2 * (host.nnz + 8)
+
+
+def test_stream_plans_cover_the_interesting_tilings(sp):
+    seen = set()
+    for case in CASES:
+        seed, N, C, K, H, W, pool, d, skew, unpadded = case
+        layer = synth.random_layer(7000 + seed, N, C, K, H, W, density=d, pool=pool, skew=skew)
+        host = sp.spconv_pack_csr(layer.w, layer.mask, H + 2, W + 2)
+        flags = sp.flags_of(True, pool) | (sp.SPCONV_UNPADDED_INPUT if unpadded else 0)
+        p = sp.spconv_plan(N, C, H, W, sp.host_csr_struct(host), K, 3, 3, 1, 1, flags,
+                           max_row_nnz=int(np.diff(host.rowptr).max()))
+        seen.add(("rpw", p["channels_per_wave"]))
+        seen.add(("chunks>1", p["chunks"] > 1))
+        seen.add(("ipw>1", p["images_per_group"] > 1))
+        seen.add(("shift", p["lds_col_shift"] != 0))
+        seen.add(("pitch!=Wp", p["lds_row_pitch"] != W + 2))
+    for want in (("rpw", 1), ("rpw", 2), ("rpw", 4), ("chunks>1", True), ("ipw>1", True), ("shift", True),
+                 ("pitch!=Wp", True)):
+        assert want in seen, want
+
+
+def test_pack_lowered_rejects_bad_input(sp):
+    lib = sp._lib
+    E = sp.SPCONV_EINVAL
+    layer = synth.random_layer(7100, 2, 8, 12, 10, 10, density=0.4)
+    host = sp.spconv_pack_csr(layer.w, layer.mask, 12, 12)
+    opt = sp.spconv_options(0, 0, None, 0, None, 0)
+    words = ctypes.c_int64()
+
+    def size(N=2, C=8, H=10, W=10, K=12, stride=1, flags=1, st=None):
+        st = sp.host_csr_struct(host) if st is None else st
+        return lib.spconv_lowered_size(N, C, H, W, ctypes.byref(st), K, 3, 3, stride, 1, flags, ctypes.byref(opt),
+                                       ctypes.byref(words))
+
+    assert size() == sp.SPCONV_OK
+    n = words.value
+    buf = np.zeros(n, np.int32)
+
+    def pack(st, cap=n):
+        return lib.spconv_pack_lowered(2, 8, 10, 10, ctypes.byref(st), 12, 3, 3, 1, 1, 1, ctypes.byref(opt),
+                                       buf.ctypes.data, cap)
+
+    assert pack(sp.host_csr_struct(host)) == sp.SPCONV_OK
+    assert pack(sp.host_csr_struct(host), n - 1) == sp.SPCONV_ECAPACITY
+    assert lib.spconv_lowered_size(2, 8, 10, 10, ctypes.byref(sp.host_csr_struct(host)), 12, 3, 3, 1, 1, 1, None,
+                                   None) == E
+    assert lib.spconv_pack_lowered(2, 8, 10, 10, ctypes.byref(sp.host_csr_struct(host)), 12, 3, 3, 1, 1, 1, None,
+                                   None, n) == E
+    # the any-stride kernel takes no stream
+    st2 = sp.spconv_csr(12, 8, 3, 3, 12, 12, host.nnz, host.rowptr.ctypes.data, host.colidx.ctypes.data,
+                        host.offset.ctypes.data, host.vals.ctypes.data)
+    assert size(stride=2, st=st2) == E
+    # invalid CSR arrays
+    for mutate in ("rowptr_decreasing", "rowptr_end", "col_range", "col_order"):
+        bad = sp.HostCSR(host.K, host.C, host.R, host.S, host.Hp, host.Wp, host.rowptr.copy(), host.colidx.copy(),
+                         host.offset.copy(), host.vals.copy())
+        if mutate == "rowptr_decreasing":
+            bad.rowptr[3] = bad.rowptr[4] + 1
+        elif mutate == "rowptr_end":
+            bad.rowptr[-1] -= 1
+        elif mutate == "col_range":
+            bad.colidx[5] = 8 * 9
+        else:
+            k = int(np.argmax(np.diff(bad.rowptr) >= 2))
+            j = int(bad.rowptr[k])
+            bad.colidx[j + 1] = bad.colidx[j]
+        assert pack(sp.host_csr_struct(bad)) == E, mutate
+
+
+def test_forward_checks_the_stream(sp):
+    lib = sp._lib
+    E = sp.SPCONV_EINVAL
+    fake = 0x1000
+    csr = sp.spconv_csr(4, 3, 3, 3, 10, 12, 5, fake, fake, fake, fake)
+    opt = sp.spconv_options(0, 0, None, 0, None, 0)
+    words = ctypes.c_int64()
+    assert lib.spconv_lowered_size(2, 3, 8, 10, ctypes.byref(csr), 4, 3, 3, 1, 1, 1, ctypes.byref(opt),
+                                   ctypes.byref(words)) == sp.SPCONV_OK
+
+    def fwd(lowered, nwords, stride=1):
+        o = sp.spconv_options(0, 0, None, 0, lowered, nwords)
+        c = csr if stride == 1 else sp.spconv_csr(4, 3, 3, 3, 10, 12, 5, fake, fake, fake, fake)
+        return lib.spconv_forward_ex(fake, 2, 3, 8, 10, ctypes.byref(c), 4, 3, 3, stride, 1, None, 1, ctypes.byref(o),
+                                     fake, None)
+
+    assert fwd(0x10000, words.value + 1) == E     # size of another plan
+    assert fwd(0x10004, words.value) == E         # not 16-byte aligned
+    assert fwd(0x10000, words.value, stride=2) == E
