@@ -289,6 +289,10 @@ int spconv_pack_lowered(int N, int C, int H, int W, const spconv_csr *csr, int K
 #define SPCONV_KERNEL_STRIDE1 1 /* stride 1: channel-chunked LDS staging, lanes own padded-width pixels */
 #define SPCONV_KERNEL_GENERIC 2 /* any stride */
 #define SPCONV_KERNEL_DENSE 3   /* dense filter on the matrix cores (spconv_forward_dense) */
+/* spconv_kernel_variants only: the stride-1 tilings also built to run several
+ * work items per workgroup with a lowered stream (the launch takes that form
+ * when the plan has more work items than launch_workgroups). */
+#define SPCONV_KERNEL_STRIDE1_TILED 4
 
 typedef struct spconv_plan_info {
     int32_t kernel;                /* SPCONV_KERNEL_STRIDE1, _GENERIC or _DENSE */
@@ -299,7 +303,7 @@ typedef struct spconv_plan_info {
     int32_t tiles_per_image;       /* spatial tiles per image */
     int32_t channels_per_chunk;    /* input channels staged in LDS at a time */
     int32_t chunks;                /* LDS chunks per tile */
-    int32_t workgroups;            /* grid size */
+    int32_t workgroups;            /* work items: (image group, spatial tile, channel tile) */
     int32_t threads_per_workgroup;
     int64_t lds_bytes;             /* dynamic LDS per workgroup */
     /* Stride-1 kernel (0 otherwise): where tap (r, s) of input channel c of a
@@ -309,6 +313,11 @@ typedef struct spconv_plan_info {
     int32_t lds_channel_floats;
     int32_t lds_row_pitch;
     int32_t lds_col_shift;
+    /* Grid of the launch: one workgroup per work item, or, for the stride-1
+     * kernel with a lowered stream (opt->lowered non-NULL; not read here)
+     * on a tiling of SPCONV_KERNEL_STRIDE1_TILED with more than 256 work
+     * items, 256 workgroups (one per CU) that take the work items in turn. */
+    int32_t launch_workgroups;
 } spconv_plan_info;
 
 /*
@@ -328,6 +337,8 @@ int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, int K, int R,
  * only), for tests and reports that must show every instance the planners can
  * pick has been run. Each instance is a 4-tuple of int32:
  *   SPCONV_KERNEL_STRIDE1  (pixels_per_lane, images_per_group, channels_per_wave, pool)
+ *   SPCONV_KERNEL_STRIDE1_TILED  the same tuple, for the tilings built to run
+ *                          several work items per workgroup
  *   SPCONV_KERNEL_GENERIC  (pixels_per_lane, 0, channels_per_workgroup, pool)
  *   SPCONV_KERNEL_DENSE    (R, S, pixel blocks per wave, pool)
  * with pool 0 or 1 and the other fields as spconv_plan_info reports them.

@@ -489,8 +489,12 @@ constexpr int kStageBlock = 256;     // floats per 16-byte-per-lane LDS DMA inst
 // instruction (buffer_load_dwordx4 ... lds). Copies may run past the tile's rows
 // into the channel's LDS padding; the buffer range stops them at the end of the
 // input tensor (such lanes read 0).
+//
+// zero_outside: with an unpadded input, also store zeros over the image
+// columns of the rows outside the image (their border), for buffers that may
+// hold another tile's rows from an earlier copy.
 __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__restrict__ xp, float *buf, int ch,
-                                               int ig, int in_row0, int wave, int lane) {
+                                               int ig, int in_row0, int wave, int lane, bool zero_outside = false) {
     const int c0 = ch * a.Cc;
     const int cn = min(a.Cc, a.C - c0);
     if (a.unpadded) {
@@ -513,6 +517,13 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
         }
         for (; cl < cn; ) {
             const int y = in_row0 + i - a.pad;
+            if (zero_outside && (y < 0 || y >= a.H)) {
+                for (int im = 0; im < a.ipw; ++im) {
+                    if (ig * a.ipw + im >= a.N) break;
+                    float *dst = buf + im * a.img_lds + cl * a.PLp + a.lds_shift + i * a.vp + a.pad;
+                    for (int x = lane; x < a.W; x += kWave) dst[x] = 0.0f;
+                }
+            }
             if (y >= 0 && y < a.H) {
                 for (int im = 0; im < a.ipw; ++im) {
                     const int nn = ig * a.ipw + im;
@@ -901,209 +912,19 @@ constexpr int lowered_pipeline_buffers() {
     return (IPW * PI <= 8 && 2 * RPW * IPW * PI + 4 * IPW * PI <= 80) ? 4 : 2;
 }
 
-// LW: the CSR rows come as a lowered entry stream (lw, see FwdArgs) instead of
-// rowptr/offset/vals: rows are assigned to waves by the stream's headers and
-// each (row, chunk) is two ready lists of (LDS index, weight) per tap parity.
-template <int PI, int IPW, int RPW, bool POOL, bool LW>
-__global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4))) void spconv_s1_kernel(
-    FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ offset,
-    const float *__restrict__ vals, const int32_t *__restrict__ lw, const float *__restrict__ bias,
-    const float *__restrict__ res, float *__restrict__ out) {
-    extern __shared__ float lds[];
-    constexpr int KT = RPW * kS1Waves;  // output channels per workgroup
-    constexpr int PJ = PI / 2;          // pixel pairs per lane per image
-    static_assert(PI % 2 == 0, "pixels per lane come in pairs");
-    constexpr int NB = pipeline_buffers<PI, IPW, RPW>();
-    constexpr bool kCompact = NB > 2;  // compacted windows where entries have few FMAs
-    constexpr int NBL = lowered_pipeline_buffers<PI, IPW, RPW>();
-
-    const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
-    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
-    const int lane = (int)threadIdx.x & 63;
-    const int kt = L % a.nktiles;
-    const int tile = L / a.nktiles;
-    const int ty = tile % a.ntiles_y;
-    const int ig = tile / a.ntiles_y;
-    const int y0 = ty * a.TH;
-    const int plane = a.Hp * a.Wp;
-
-    // Output channels of this wave. With RPW > 1 the workgroup's KT channels
-    // are ranked by nonzero count and dealt to the waves in snake order (ranks
-    // w, 2*16-1-w, 2*16+w, ...), so heavy and light channels share a wave and
-    // the waves' loads even out.
-    int krow[RPW];
-    // Lowered stream: the header of (row slot i, chunk ch) of this wave, and
-    // the entries after all headers.
-    const int32_t *lw_ent = LW ? lw + 4 * (size_t)a.lw_headers : nullptr;
-    const int hslot = (kt * kS1Waves + wave) * RPW;
-    auto lw_header = [&](int i, int ch) {
-        return *reinterpret_cast<const int4 *>(lw + 4 * (size_t)((hslot + i) * a.nchunks + ch));
-    };
-    int4 lwh[RPW];
-    if constexpr (LW) {
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            lwh[i] = lw_header(i, 0);
-            krow[i] = lwh[i].w;
-        }
-    } else if constexpr (RPW == 1) {
-        krow[0] = kt * KT + wave;
-    } else {
-        const int k0 = kt * KT;
-        int nz = -1;
-        if (lane < KT && k0 + lane < a.K) nz = rowptr[k0 + lane + 1] - rowptr[k0 + lane];
-        int rank = 0;
-        for (int j = 0; j < KT; ++j) {
-            const int o = __builtin_amdgcn_readlane(nz, j);
-            rank += (o > nz || (o == nz && j < lane)) ? 1 : 0;
-        }
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            const int want = i * kS1Waves + ((i & 1) ? kS1Waves - 1 - wave : wave);
-            const unsigned long long m = __builtin_amdgcn_ballot_w64(lane < KT && rank == want);
-            krow[i] = k0 + (int)__builtin_ctzll(m);
-        }
-    }
-    int cur[RPW], end[RPW];
-#pragma unroll
-    for (int i = 0; i < RPW; ++i) {
-        const int k = krow[i];
-        cur[i] = (!LW && k < a.K) ? rowptr[k] : 0;
-        end[i] = (!LW && k < a.K) ? rowptr[k + 1] : 0;
-    }
-
-    // accE: pixels (2l + 128j, 2l+1 + 128j) from even taps; accO: pixels
-    // (2l-1 + 128j, 2l + 128j) from odd taps.
-    float2 accE[RPW][IPW][PJ], accO[RPW][IPW][PJ];
-#pragma unroll
-    for (int i = 0; i < RPW; ++i)
-#pragma unroll
-        for (int im = 0; im < IPW; ++im)
-#pragma unroll
-            for (int p = 0; p < PJ; ++p) {
-                accE[i][im][p] = make_float2(0.0f, 0.0f);
-                accO[i][im][p] = make_float2(0.0f, 0.0f);
-            }
-
-    // LDS float index of tap offset o for chunk ch, pixel q: vb(ch) + o - c*plane_delta + q.
-    auto vb_of = [&](int ch) { return (ch & 1) * a.buf_floats - ch * a.Cc * a.PLp; };
-    auto bound_of = [&](int ch) { return min((ch + 1) * a.Cc, a.C) * plane; };
+// Epilogue of one tile of the stride-1 kernel: bias, residual, ReLU, then the
+// stores (or the 2x2 pool through a wave-private LDS staging tile), and the
+// zero border of bordered outputs. accE/accO hold the even- and odd-tap sums of
+// the wave's RPW channels krow over the tile (images ig*IPW.., rows y0..).
+// The pooled form reuses the chunk buffers: every wave must be past its last
+// read of them (a barrier) before the call.
+template <int PI, int IPW, int RPW, bool POOL>
+__device__ __forceinline__ void s1_epilogue(const FwdArgs &a, float2 (&accE)[RPW][IPW][PI / 2],
+                                            float2 (&accO)[RPW][IPW][PI / 2], const int (&krow)[RPW], int ig, int ty,
+                                            int y0, int wave, int lane, float *lds, const float *__restrict__ bias,
+                                            const float *__restrict__ res, float *__restrict__ out) {
+    constexpr int PJ = PI / 2;
     const int q = 2 * lane;
-
-    Window<kCompact> win[RPW];
-    RawWindow next[RPW];
-    if (a.unpadded) {
-        // Zero both chunk buffers once: the staging of an unpadded input never
-        // writes the border positions, which must read as the zero padding.
-        for (int e = (int)threadIdx.x * 4; e < 2 * a.buf_floats; e += kS1Threads * 4)
-            *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        __syncthreads();
-    }
-    stage_chunk_s1(a, xp, lds, 0, ig, y0, wave, lane);
-    if constexpr (!LW) {
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
-            win[i] = decode_window<kCompact>(a, next[i], end[i], bound_of(0), vb_of(0), lane);
-        }
-    }
-    wait_async_copies();
-    __syncthreads();
-
-    for (int ch = 0; ch < a.nchunks; ++ch) {
-        const bool more = ch + 1 < a.nchunks;
-        if constexpr (LW) {
-            if (more) stage_chunk_s1(a, xp, lds + ((ch + 1) & 1) * a.buf_floats, ch + 1, ig, y0, wave, lane);
-            // Entry lists of this chunk, clamped to the stream.
-            int st[RPW], ne[RPW], no[RPW];
-            int total = 0, done = 0;
-#pragma unroll
-            for (int i = 0; i < RPW; ++i) {
-                st[i] = min(max(lwh[i].x, 0), a.lw_entries);
-                ne[i] = min(max(lwh[i].y, 0), a.lw_entries - st[i]);
-                no[i] = min(max(lwh[i].z, 0), a.lw_entries - st[i] - ne[i]);
-                total += ne[i] + no[i];
-            }
-            const int qv = (ch & 1) * a.buf_floats + q;
-            set_progress_prio(0, total);
-#pragma unroll
-            for (int i = 0; i < RPW; ++i) {
-                run_lowered<NBL>(accE[i], lw_ent, st[i], ne[i], lds, qv, a.img_lds);
-                done += ne[i];
-                set_progress_prio(done, total);
-                run_lowered<NBL>(accO[i], lw_ent, st[i] + ne[i], no[i], lds, qv, a.img_lds);
-                done += no[i];
-                set_progress_prio(done, total);
-            }
-            if (more) {
-#pragma unroll
-                for (int i = 0; i < RPW; ++i) lwh[i] = lw_header(i, ch + 1);
-            }
-            if (POOL || more) {
-                wait_async_copies();
-                __syncthreads();
-            }
-            continue;
-        }
-        if (more) {
-            stage_chunk_s1(a, xp, lds + ((ch + 1) & 1) * a.buf_floats, ch + 1, ig, y0, wave, lane);
-            // Fetch the next chunk's windows now, from where this chunk's
-            // entries end, so their latency hides behind this chunk's work.
-#pragma unroll
-            for (int i = 0; i < RPW; ++i) next[i] = fetch_window(offset, vals, cur[i] + win[i].n, end[i], lane);
-        }
-        const int bound = bound_of(ch);
-        const int vb = vb_of(ch);
-        int total = 0, done = 0;
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) total += win[i].n;
-        set_progress_prio(0, total);
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-            for (;;) {
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    if constexpr (kCompact) {
-                        const int ne = win[i].ne[h], no = win[i].no[h];
-                        run_range<NB>(accE[i], win[i].lo[h], win[i].w[h], 0, ne, lds, q, a.img_lds);
-                        done += ne;
-                        set_progress_prio(done, total);
-                        run_range<NB>(accO[i], win[i].lo[h], win[i].w[h], ne, ne + no, lds, q, a.img_lds);
-                        done += no;
-                    } else {
-                        run_mask<NB>(accE[i], win[i].lo[h], win[i].w[h], win[i].even[h], lds, q, a.img_lds);
-                        done += __builtin_popcountll(win[i].even[h]);
-                        set_progress_prio(done, total);
-                        run_mask<NB>(accO[i], win[i].lo[h], win[i].w[h], win[i].odd[h], lds, q, a.img_lds);
-                        done += __builtin_popcountll(win[i].odd[h]);
-                    }
-                    set_progress_prio(done, total);
-                }
-                const int n = win[i].n;
-                cur[i] += n;
-                if (n < 2 * kWave || cur[i] >= end[i]) break;
-                // The row has more entries in this chunk than one window holds.
-                win[i] = decode_window<kCompact>(a, fetch_window(offset, vals, cur[i], end[i], lane), end[i], bound,
-                                                 vb, lane);
-            }
-        }
-        if (more) {
-#pragma unroll
-            for (int i = 0; i < RPW; ++i) {
-                // A row that overflowed a window in this chunk ends elsewhere.
-                if (next[i].base != cur[i]) next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
-                win[i] = decode_window<kCompact>(a, next[i], end[i], bound_of(ch + 1), vb_of(ch + 1), lane);
-            }
-        }
-        // Chunk ch+1 is in LDS and every wave is done with chunk ch's buffer.
-        // After the last chunk only the pooled epilogue, which reuses the
-        // buffers, needs the barrier.
-        if (POOL || more) {
-            wait_async_copies();
-            __syncthreads();
-        }
-    }
-
     const int tile_px = a.TH * a.vp;
     if constexpr (!POOL) {
         // Tile row of each of this lane's pixels, or -1 when the pixel is not
@@ -1243,6 +1064,309 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
             }
         }
     }
+}
+
+// Stride-1 kernel with a lowered entry stream (see FwdArgs): the workgroup
+// takes work items (channel tile, spatial tile, image group) b, b + G, b + 2G,
+// ... of the T = a.total_wgs items in the grid of G workgroups (one per CU
+// when T exceeds the CUs), so the copies and stores at a tile's edges overlap
+// the arithmetic of its neighbours: the chunk copies run as one stream across
+// tiles (chunk buffer = global chunk count & 1), the next tile's first chunk
+// is copied during the current tile's last chunk, and the current tile's
+// stores drain while the next tile computes. With the pooled epilogue, whose
+// staging tile reuses the chunk buffers, the next tile's first copy follows
+// the epilogue. At iteration t the workgroup takes item t*G + its XCD-ordered
+// index within that round, so the workgroups of one XCD work on neighbouring
+// tiles (shared input rows in that XCD's L2), as in a one-tile-per-workgroup
+// grid.
+template <int PI, int IPW, int RPW, bool POOL, bool PERSIST>
+__device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *__restrict__ xp,
+                                                 const int32_t *__restrict__ lw, const float *__restrict__ bias,
+                                                 const float *__restrict__ res, float *__restrict__ out, float *lds) {
+    constexpr int PJ = PI / 2;
+    constexpr int NBL = lowered_pipeline_buffers<PI, IPW, RPW>();
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    const int lane = (int)threadIdx.x & 63;
+    const int q = 2 * lane;
+    const int G = (int)gridDim.x, T = a.total_wgs, b = (int)blockIdx.x;
+    const int32_t *ent = lw + 4 * (size_t)a.lw_headers;
+    auto header = [&](int kt, int i, int ch) {
+        return *reinterpret_cast<const int4 *>(lw + 4 * (size_t)(((kt * kS1Waves + wave) * RPW + i) * a.nchunks + ch));
+    };
+    struct Item {
+        int kt, ty, ig;
+    };
+    // Round it holds items it*G .. min((it+1)*G, T) - 1; workgroup b takes
+    // the one at its XCD-ordered position among that round's (b is below
+    // the round's size whenever the round has an item for it).
+    auto item_of = [&](int it) {
+        const int L = it * G + xcd_linear_id(b, min(G, T - it * G));
+        Item r;
+        r.kt = L % a.nktiles;
+        const int t = L / a.nktiles;
+        r.ty = t % a.ntiles_y;
+        r.ig = t / a.ntiles_y;
+        return r;
+    };
+    if (b >= T) return;
+    if (a.unpadded) {
+        // The border columns of both buffers stay zero for every tile (no copy
+        // writes them); rows outside the image are zeroed by each staging.
+        for (int e = (int)threadIdx.x * 4; e < 2 * a.buf_floats; e += kS1Threads * 4)
+            *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        __syncthreads();
+    }
+    Item cur = item_of(0);
+    stage_chunk_s1(a, xp, lds, 0, cur.ig, cur.ty * a.TH, wave, lane, PERSIST);
+    wait_async_copies();
+    __syncthreads();
+    int sbuf = 0;  // buffer of the chunk being computed
+    for (int it = 0;; ++it) {
+        const bool has_next = PERSIST && (it + 1) * G + b < T;
+        const Item nxt = has_next ? item_of(it + 1) : cur;
+        const int y0 = cur.ty * a.TH;
+        int krow[RPW];
+        int4 h[RPW];
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            h[i] = header(cur.kt, i, 0);
+            krow[i] = h[i].w;
+        }
+        float2 accE[RPW][IPW][PJ], accO[RPW][IPW][PJ];
+#pragma unroll
+        for (int i = 0; i < RPW; ++i)
+#pragma unroll
+            for (int im = 0; im < IPW; ++im)
+#pragma unroll
+                for (int pp = 0; pp < PJ; ++pp) {
+                    accE[i][im][pp] = make_float2(0.0f, 0.0f);
+                    accO[i][im][pp] = make_float2(0.0f, 0.0f);
+                }
+        for (int ch = 0; ch < a.nchunks; ++ch) {
+            const bool more = ch + 1 < a.nchunks;
+            float *nbuf = lds + (sbuf ^ 1) * a.buf_floats;
+            if (more)
+                stage_chunk_s1(a, xp, nbuf, ch + 1, cur.ig, y0, wave, lane, PERSIST);
+            else if (!POOL && has_next)
+                stage_chunk_s1(a, xp, nbuf, 0, nxt.ig, nxt.ty * a.TH, wave, lane, PERSIST);
+            // Entry lists of this chunk, clamped to the stream.
+            int st[RPW], ne[RPW], no[RPW];
+            int total = 0, done = 0;
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) {
+                st[i] = min(max(h[i].x, 0), a.lw_entries);
+                ne[i] = min(max(h[i].y, 0), a.lw_entries - st[i]);
+                no[i] = min(max(h[i].z, 0), a.lw_entries - st[i] - ne[i]);
+                total += ne[i] + no[i];
+            }
+            const int qv = sbuf * a.buf_floats + q;
+            set_progress_prio(0, total);
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) {
+                run_lowered<NBL>(accE[i], ent, st[i], ne[i], lds, qv, a.img_lds);
+                done += ne[i];
+                set_progress_prio(done, total);
+                run_lowered<NBL>(accO[i], ent, st[i] + ne[i], no[i], lds, qv, a.img_lds);
+                done += no[i];
+                set_progress_prio(done, total);
+            }
+            if (more) {
+#pragma unroll
+                for (int i = 0; i < RPW; ++i) h[i] = header(cur.kt, i, ch + 1);
+            }
+            // The next chunk (or the next tile's first) is in LDS and every
+            // wave is done with this chunk's buffer (or, before the pooled
+            // epilogue, with both).
+            if (more || POOL || has_next) {
+                wait_async_copies();
+                __syncthreads();
+            }
+            sbuf ^= 1;
+        }
+        s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, cur.ig, cur.ty, y0, wave, lane, lds, bias, res, out);
+        if (!has_next) break;
+        if constexpr (POOL) {
+            // The staging tile overlaps the buffers: the next tile's first
+            // chunk is copied after every wave's pooled stores. With an
+            // unpadded input the staging also overwrote border positions that
+            // no copy rewrites: they are zeroed again first.
+            __syncthreads();
+            if (a.unpadded) {
+                const int staged = kS1Waves * IPW * kWave * PI;
+                for (int e = (int)threadIdx.x * 4; e < staged; e += kS1Threads * 4)
+                    *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                __syncthreads();
+            }
+            stage_chunk_s1(a, xp, lds + sbuf * a.buf_floats, 0, nxt.ig, nxt.ty * a.TH, wave, lane, true);
+            wait_async_copies();
+            __syncthreads();
+        }
+        cur = nxt;
+    }
+}
+
+// MODE: kModePlain walks the CSR rows (rowptr/offset/vals); kModeLowered and
+// kModeTiled read the lowered entry stream (lw, see FwdArgs) instead: rows are
+// assigned to waves by the stream's headers and each (row, chunk) is two
+// ready lists of (LDS index, weight) per tap parity; kModeTiled runs several
+// work items per workgroup (s1_lowered_tiles).
+constexpr int kModePlain = 0, kModeLowered = 1, kModeTiled = 2;
+
+template <int PI, int IPW, int RPW, bool POOL, int MODE>
+__global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4))) void spconv_s1_kernel(
+    FwdArgs a, const float *__restrict__ xp, const int32_t *__restrict__ rowptr, const int32_t *__restrict__ offset,
+    const float *__restrict__ vals, const int32_t *__restrict__ lw, const float *__restrict__ bias,
+    const float *__restrict__ res, float *__restrict__ out) {
+    extern __shared__ float lds[];
+    constexpr int KT = RPW * kS1Waves;  // output channels per workgroup
+    constexpr int PJ = PI / 2;          // pixel pairs per lane per image
+    static_assert(PI % 2 == 0, "pixels per lane come in pairs");
+    constexpr int NB = pipeline_buffers<PI, IPW, RPW>();
+    constexpr bool kCompact = NB > 2;  // compacted windows where entries have few FMAs
+    if constexpr (MODE != kModePlain) {
+        s1_lowered_tiles<PI, IPW, RPW, POOL, MODE == kModeTiled>(a, xp, lw, bias, res, out, lds);
+        return;
+    }
+
+    const int L = xcd_linear_id((int)blockIdx.x, a.total_wgs);
+    const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+    const int lane = (int)threadIdx.x & 63;
+    const int kt = L % a.nktiles;
+    const int tile = L / a.nktiles;
+    const int ty = tile % a.ntiles_y;
+    const int ig = tile / a.ntiles_y;
+    const int y0 = ty * a.TH;
+    const int plane = a.Hp * a.Wp;
+
+    // Output channels of this wave. With RPW > 1 the workgroup's KT channels
+    // are ranked by nonzero count and dealt to the waves in snake order (ranks
+    // w, 2*16-1-w, 2*16+w, ...), so heavy and light channels share a wave and
+    // the waves' loads even out.
+    int krow[RPW];
+    if constexpr (RPW == 1) {
+        krow[0] = kt * KT + wave;
+    } else {
+        const int k0 = kt * KT;
+        int nz = -1;
+        if (lane < KT && k0 + lane < a.K) nz = rowptr[k0 + lane + 1] - rowptr[k0 + lane];
+        int rank = 0;
+        for (int j = 0; j < KT; ++j) {
+            const int o = __builtin_amdgcn_readlane(nz, j);
+            rank += (o > nz || (o == nz && j < lane)) ? 1 : 0;
+        }
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int want = i * kS1Waves + ((i & 1) ? kS1Waves - 1 - wave : wave);
+            const unsigned long long m = __builtin_amdgcn_ballot_w64(lane < KT && rank == want);
+            krow[i] = k0 + (int)__builtin_ctzll(m);
+        }
+    }
+    int cur[RPW], end[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+        const int k = krow[i];
+        cur[i] = (k < a.K) ? rowptr[k] : 0;
+        end[i] = (k < a.K) ? rowptr[k + 1] : 0;
+    }
+
+    // accE: pixels (2l + 128j, 2l+1 + 128j) from even taps; accO: pixels
+    // (2l-1 + 128j, 2l + 128j) from odd taps.
+    float2 accE[RPW][IPW][PJ], accO[RPW][IPW][PJ];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i)
+#pragma unroll
+        for (int im = 0; im < IPW; ++im)
+#pragma unroll
+            for (int p = 0; p < PJ; ++p) {
+                accE[i][im][p] = make_float2(0.0f, 0.0f);
+                accO[i][im][p] = make_float2(0.0f, 0.0f);
+            }
+
+    // LDS float index of tap offset o for chunk ch, pixel q: vb(ch) + o - c*plane_delta + q.
+    auto vb_of = [&](int ch) { return (ch & 1) * a.buf_floats - ch * a.Cc * a.PLp; };
+    auto bound_of = [&](int ch) { return min((ch + 1) * a.Cc, a.C) * plane; };
+    const int q = 2 * lane;
+
+    Window<kCompact> win[RPW];
+    RawWindow next[RPW];
+    if (a.unpadded) {
+        // Zero both chunk buffers once: the staging of an unpadded input never
+        // writes the border positions, which must read as the zero padding.
+        for (int e = (int)threadIdx.x * 4; e < 2 * a.buf_floats; e += kS1Threads * 4)
+            *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+        __syncthreads();
+    }
+    stage_chunk_s1(a, xp, lds, 0, ig, y0, wave, lane);
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+        next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
+        win[i] = decode_window<kCompact>(a, next[i], end[i], bound_of(0), vb_of(0), lane);
+    }
+    wait_async_copies();
+    __syncthreads();
+
+    for (int ch = 0; ch < a.nchunks; ++ch) {
+        const bool more = ch + 1 < a.nchunks;
+        if (more) {
+            stage_chunk_s1(a, xp, lds + ((ch + 1) & 1) * a.buf_floats, ch + 1, ig, y0, wave, lane);
+            // Fetch the next chunk's windows now, from where this chunk's
+            // entries end, so their latency hides behind this chunk's work.
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) next[i] = fetch_window(offset, vals, cur[i] + win[i].n, end[i], lane);
+        }
+        const int bound = bound_of(ch);
+        const int vb = vb_of(ch);
+        int total = 0, done = 0;
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) total += win[i].n;
+        set_progress_prio(0, total);
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            for (;;) {
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    if constexpr (kCompact) {
+                        const int ne = win[i].ne[h], no = win[i].no[h];
+                        run_range<NB>(accE[i], win[i].lo[h], win[i].w[h], 0, ne, lds, q, a.img_lds);
+                        done += ne;
+                        set_progress_prio(done, total);
+                        run_range<NB>(accO[i], win[i].lo[h], win[i].w[h], ne, ne + no, lds, q, a.img_lds);
+                        done += no;
+                    } else {
+                        run_mask<NB>(accE[i], win[i].lo[h], win[i].w[h], win[i].even[h], lds, q, a.img_lds);
+                        done += __builtin_popcountll(win[i].even[h]);
+                        set_progress_prio(done, total);
+                        run_mask<NB>(accO[i], win[i].lo[h], win[i].w[h], win[i].odd[h], lds, q, a.img_lds);
+                        done += __builtin_popcountll(win[i].odd[h]);
+                    }
+                    set_progress_prio(done, total);
+                }
+                const int n = win[i].n;
+                cur[i] += n;
+                if (n < 2 * kWave || cur[i] >= end[i]) break;
+                // The row has more entries in this chunk than one window holds.
+                win[i] = decode_window<kCompact>(a, fetch_window(offset, vals, cur[i], end[i], lane), end[i], bound,
+                                                 vb, lane);
+            }
+        }
+        if (more) {
+#pragma unroll
+            for (int i = 0; i < RPW; ++i) {
+                // A row that overflowed a window in this chunk ends elsewhere.
+                if (next[i].base != cur[i]) next[i] = fetch_window(offset, vals, cur[i], end[i], lane);
+                win[i] = decode_window<kCompact>(a, next[i], end[i], bound_of(ch + 1), vb_of(ch + 1), lane);
+            }
+        }
+        // Chunk ch+1 is in LDS and every wave is done with chunk ch's buffer.
+        // After the last chunk only the pooled epilogue, which reuses the
+        // buffers, needs the barrier.
+        if (POOL || more) {
+            wait_async_copies();
+            __syncthreads();
+        }
+    }
+
+    s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, ig, ty, y0, wave, lane, lds, bias, res, out);
 }
 
 // Generic-stride kernel: waves split the pixels of the tile and every wave
@@ -1453,6 +1577,12 @@ using FwdKernel = void (*)(FwdArgs, const float *, const int32_t *, const int32_
 struct S1Variant {
     int pi, ipw, rpw, pools;
 };
+
+// Tilings also built to run several work items per workgroup with a lowered
+// stream: those of large planes (one image per tile, many pixels per lane),
+// whose grids run many rounds of workgroups. Other tilings keep one work item
+// per workgroup, which holds fewer registers.
+constexpr bool tiled_variant(const S1Variant &v) { return v.ipw == 1 && v.pi >= 12; }
 constexpr S1Variant kS1Variants[] = {
     // one image per tile
     {24, 1, 1, 3}, {22, 1, 1, 3}, {20, 1, 1, 3}, {18, 1, 1, 3}, {16, 1, 1, 3}, {14, 1, 1, 3}, {12, 1, 1, 3},
@@ -1470,27 +1600,32 @@ constexpr S1Variant kS1Variants[] = {
 };
 constexpr int kNumS1Variants = (int)(sizeof(kS1Variants) / sizeof(kS1Variants[0]));
 
+template <int PI, int IPW, int RPW, bool POOL, bool TILED>
+FwdKernel pick_s1_mode(int mode) {
+    if (mode == kModePlain) return spconv_s1_kernel<PI, IPW, RPW, POOL, kModePlain>;
+    if (mode == kModeLowered) return spconv_s1_kernel<PI, IPW, RPW, POOL, kModeLowered>;
+    if constexpr (TILED) return spconv_s1_kernel<PI, IPW, RPW, POOL, kModeTiled>;
+    return nullptr;
+}
+
 template <int I>
-FwdKernel pick_s1_from(int PI, int IPW, int RPW, bool pool, bool lowered) {
+FwdKernel pick_s1_from(int PI, int IPW, int RPW, bool pool, int mode) {
     if constexpr (I == kNumS1Variants) {
         return nullptr;
     } else {
         constexpr S1Variant v = kS1Variants[I];
         static_assert(v.ipw * v.pi <= 24 && v.rpw * v.ipw * v.pi <= 32 && v.pi % 2 == 0,
                       "tiling exceeds the register budget");
+        constexpr bool tiled = tiled_variant(v);
         if (v.pi == PI && v.ipw == IPW && v.rpw == RPW) {
             if (pool) {
-                if constexpr ((v.pools & 2) != 0)
-                    return lowered ? spconv_s1_kernel<v.pi, v.ipw, v.rpw, true, true>
-                                   : spconv_s1_kernel<v.pi, v.ipw, v.rpw, true, false>;
+                if constexpr ((v.pools & 2) != 0) return pick_s1_mode<v.pi, v.ipw, v.rpw, true, tiled>(mode);
                 return nullptr;
             }
-            if constexpr ((v.pools & 1) != 0)
-                return lowered ? spconv_s1_kernel<v.pi, v.ipw, v.rpw, false, true>
-                               : spconv_s1_kernel<v.pi, v.ipw, v.rpw, false, false>;
+            if constexpr ((v.pools & 1) != 0) return pick_s1_mode<v.pi, v.ipw, v.rpw, false, tiled>(mode);
             return nullptr;
         }
-        return pick_s1_from<I + 1>(PI, IPW, RPW, pool, lowered);
+        return pick_s1_from<I + 1>(PI, IPW, RPW, pool, mode);
     }
 }
 
@@ -1499,8 +1634,8 @@ FwdKernel pick_s1_from(int PI, int IPW, int RPW, bool pool, bool lowered) {
 constexpr int kPiSingle[] = {24, 22, 20, 18, 16, 14, 12, 10, 8, 6, 4};
 constexpr int kPiMulti[] = {8, 6, 4, 2};
 
-FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool, bool lowered = false) {
-    return pick_s1_from<0>(PI, IPW, RPW, pool, lowered);
+FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool, int mode = kModePlain) {
+    return pick_s1_from<0>(PI, IPW, RPW, pool, mode);
 }
 
 // Picks the stride-1 tiling with the smallest modelled run time. The model
@@ -1679,10 +1814,11 @@ bool plan_generic(int N, int C, int K, int Hp, int Wp, int Ho, int Wo, int strid
     return true;
 }
 
-FwdKernel pick_kernel(const Plan &pl, bool pool, bool lowered = false) {
+FwdKernel pick_kernel(const Plan &pl, bool pool, int mode = kModePlain) {
     if (pl.kind == Kind::kGeneric)
-        return lowered ? nullptr : (pool ? spconv_generic_kernel<4, 4, true> : spconv_generic_kernel<4, 4, false>);
-    return pick_s1(pl.PI, pl.IPW, pl.RPW, pool, lowered);
+        return mode != kModePlain ? nullptr
+                                  : (pool ? spconv_generic_kernel<4, 4, true> : spconv_generic_kernel<4, 4, false>);
+    return pick_s1(pl.PI, pl.IPW, pl.RPW, pool, mode);
 }
 
 bool out_extent(int in, int f, int stride, int pad, int *o) {
@@ -1937,6 +2073,21 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
 
 // Border and residual options of spconv_forward_ex, checked and folded into
 // the args.
+// Kernel mode of a launch: the plain CSR walk, or with a lowered stream the
+// one-item-per-workgroup form, or, where the tiling is built for it and there
+// are more work items than one round of workgroups (one per CU of MI355X,
+// each holding the CU's whole LDS), the form that runs several items per
+// workgroup and overlaps tile edges.
+constexpr int kResidentWgs = 256;
+int launch_mode(const Plan &pl, bool lowered, bool pool) {
+    if (!lowered || pl.kind != Kind::kStride1) return kModePlain;
+    if (pl.total_wgs > kResidentWgs && pick_s1(pl.PI, pl.IPW, pl.RPW, pool, kModeTiled)) return kModeTiled;
+    return kModeLowered;
+}
+int launch_grid(const Plan &pl, int mode) {
+    return mode == kModeTiled ? std::min(pl.total_wgs, kResidentWgs) : pl.total_wgs;
+}
+
 // Lowered stream of a stride-1 plan: headers (4 words each) per (channel
 // tile, wave, row slot, chunk), then nnz entries and kLwPad pad entries (2
 // words each).
@@ -1990,7 +2141,8 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
         a.lw_headers = lowered_headers(pl);
         a.lw_entries = (int)csr->nnz;
     }
-    FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0, lowered != nullptr);
+    const int mode = launch_mode(pl, lowered != nullptr, (flags & SPCONV_MAXPOOL2X2) != 0);
+    FwdKernel kern = pick_kernel(pl, (flags & SPCONV_MAXPOOL2X2) != 0, mode);
     if (!kern) return SPCONV_EINVAL;
     const unsigned threads = pl.kind == Kind::kStride1 ? kS1Threads : kThreads;
     // Each kernel instance's dynamic-LDS limit is raised once, to the most any
@@ -1998,8 +2150,8 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
     // several host threads never lower it under one another.
     if (!raise_lds_limit((const void *)kern, pl.kind == Kind::kStride1 ? kS1LdsFloats * 4 : kGenericLdsBytes))
         return SPCONV_EHIP;
-    hipLaunchKernelGGL(kern, dim3((unsigned)pl.total_wgs), dim3(threads), pl.lds_bytes, stream, a, in_padded,
-                       csr->rowptr, csr->offset, csr->vals, lowered, bias, residual, out);
+    hipLaunchKernelGGL(kern, dim3((unsigned)launch_grid(pl, mode)), dim3(threads), pl.lds_bytes, stream, a,
+                       in_padded, csr->rowptr, csr->offset, csr->vals, lowered, bias, residual, out);
     return hipGetLastError() == hipSuccess ? SPCONV_OK : SPCONV_EHIP;
 }
 
@@ -2033,13 +2185,16 @@ extern "C" int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, in
     info->lds_channel_floats = s1 ? pl.PLp : 0;
     info->lds_row_pitch = s1 ? a.vp : 0;
     info->lds_col_shift = s1 ? a.lds_shift : 0;
+    info->launch_workgroups =
+        launch_grid(pl, launch_mode(pl, opt && opt->lowered, (flags & SPCONV_MAXPOOL2X2) != 0));
     return SPCONV_OK;
 }
 
 extern "C" int spconv_kernel_variants(int32_t kernel, int32_t *variants, int32_t capacity, int32_t *count) {
     if (!count || capacity < 0 || (capacity > 0 && !variants)) return SPCONV_EINVAL;
     if (kernel == SPCONV_KERNEL_DENSE) return dense_kernel_variants(variants, capacity, count);
-    if (kernel != SPCONV_KERNEL_STRIDE1 && kernel != SPCONV_KERNEL_GENERIC) return SPCONV_EINVAL;
+    if (kernel != SPCONV_KERNEL_STRIDE1 && kernel != SPCONV_KERNEL_GENERIC && kernel != SPCONV_KERNEL_STRIDE1_TILED)
+        return SPCONV_EINVAL;
     int n = 0;
     auto put = [&](int a, int b, int c, int d) {
         if (n < capacity) {
@@ -2056,7 +2211,8 @@ extern "C" int spconv_kernel_variants(int32_t kernel, int32_t *variants, int32_t
     } else {
         for (const S1Variant &v : kS1Variants)
             for (int pool = 0; pool < 2; ++pool)
-                if (v.pools & (1 << pool)) put(v.pi, v.ipw, v.rpw, pool);
+                if ((v.pools & (1 << pool)) && (kernel == SPCONV_KERNEL_STRIDE1 || tiled_variant(v)))
+                    put(v.pi, v.ipw, v.rpw, pool);
     }
     *count = n;
     return SPCONV_OK;

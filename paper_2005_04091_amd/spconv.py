@@ -32,6 +32,7 @@ EXPORTED = ("spconv_pack_csr", "spconv_pad_input", "spconv_resize_pad_input", "s
 SPCONV_KERNEL_STRIDE1 = 1
 SPCONV_KERNEL_GENERIC = 2
 SPCONV_KERNEL_DENSE = 3
+SPCONV_KERNEL_STRIDE1_TILED = 4
 SPCONV_PATH_SPARSE = 1
 SPCONV_PATH_DENSE = 2
 
@@ -57,7 +58,7 @@ class spconv_plan_info(ctypes.Structure):
                 ("tiles_per_image", ctypes.c_int32), ("channels_per_chunk", ctypes.c_int32),
                 ("chunks", ctypes.c_int32), ("workgroups", ctypes.c_int32), ("threads_per_workgroup", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int64), ("lds_channel_floats", ctypes.c_int32), ("lds_row_pitch", ctypes.c_int32),
-                ("lds_col_shift", ctypes.c_int32)]
+                ("lds_col_shift", ctypes.c_int32), ("launch_workgroups", ctypes.c_int32)]
 
 
 _c_int = ctypes.c_int
@@ -413,15 +414,16 @@ def spconv_forward_dense(xp, N: int, C: int, H: int, W: int, packed, K: int, R: 
 
 
 def spconv_plan(N: int, C: int, H: int, W: int, csr, K: int, R: int, S: int, stride: int, pad: int,
-                flags: int = SPCONV_RELU, max_row_nnz: int | None = None) -> dict:
+                flags: int = SPCONV_RELU, max_row_nnz: int | None = None, lowered: bool = False) -> dict:
     """The launch plan ``spconv_forward_ex`` would use, as a dict of the
     ``spconv_plan_info`` fields. ``csr`` is a DeviceCSR (its arrays are not
     read; the hint defaults to its measured max_row_nnz) or a bare
-    ``spconv_csr`` struct (hint default 0)."""
+    ``spconv_csr`` struct (hint default 0); ``lowered``: the call passes a
+    lowered stream (only its presence matters to the plan)."""
     struct = csr.struct if isinstance(csr, DeviceCSR) else csr
     if max_row_nnz is None:
         max_row_nnz = csr.max_row_nnz if isinstance(csr, DeviceCSR) else 0
-    opt = spconv_options(0, 0, None, max_row_nnz, None, 0)
+    opt = spconv_options(0, 0, None, max_row_nnz, 16 if lowered else None, 0)
     info = spconv_plan_info()
     _check(_lib.spconv_plan(N, C, H, W, ctypes.byref(struct), K, R, S, stride, pad, flags, ctypes.byref(opt),
                             ctypes.byref(info)), "spconv_plan")
@@ -570,8 +572,11 @@ class SparseConvLayer:
     def plan(self, N: int) -> dict:
         if self.path == "dense":
             return spconv_dense_plan(N, self.C, self.H, self.W, self.K, self.R, self.S, self.pad, self.flags)
+        lw = self.path == "sparse" and self.use_lowered and spconv_plan(
+            N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride, self.pad,
+            self.flags)["kernel"] == SPCONV_KERNEL_STRIDE1
         return spconv_plan(N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride, self.pad,
-                           self.flags)
+                           self.flags, lowered=lw)
 
     def run(self, x, xp=None, out=None, stream=None):
         xp = self.pad_input(x, out=xp, stream=stream)

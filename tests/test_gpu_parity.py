@@ -259,6 +259,10 @@ VARIANTS = [
     ("ipw1_rpw2_pool_chunks_overflow", 8, 250, 520, 12, True, True, (4, 1, 2)),
     ("ipw4_rpw1_pool", 16, 3, 520, 2, True, False, (2, 4, 1)),
     ("ipw4_rpw2_pool", 32, 3, 520, 2, True, False, (2, 4, 2)),
+    # more work items than CUs, the last round partly filled (495 items): the
+    # lowered kernel runs several work items per workgroup
+    ("ipw1_rpw1_495_items", 33, 3, 48, 64, False, False, (14, 1, 1)),
+    ("ipw1_rpw1_pool_495_items", 33, 3, 48, 56, True, False, (12, 1, 1)),
 ]
 
 
@@ -273,6 +277,8 @@ def test_kernel_variant(sp, case):
     assert (plan["pixels_per_lane"], plan["images_per_group"], plan["channels_per_wave"]) == expect
     if "chunks" in name:
         assert plan["chunks"] >= 2, "the variant must span several LDS chunks"
+    if "items" in name:
+        assert plan["workgroups"] > plan["launch_workgroups"] == 256 and plan["workgroups"] % 256
     out = L.run(torch.from_numpy(layer.x).cuda())
     torch.cuda.synchronize()
     ref, ab = oracle_layer(layer)

@@ -41,8 +41,9 @@ def check_close(gpu, ref, ab, what):
 @pytest.mark.parametrize("case", vc.CASES, ids=[f"{c[0]}{c[1]}" for c in vc.CASES])
 def test_instance_against_oracle(sp, case):
     """Each instance against the oracle; stride-1 instances in both forms (the
-    plain CSR walk and the lowered entry stream), which must agree bit for
-    bit (same entries, same summation order)."""
+    plain CSR walk and the lowered entry stream, for "s1t" cases in its form
+    with several work items per workgroup), which must agree bit for bit
+    (same entries, same summation order)."""
     import torch
     kind, variant, N, C, K, H, W, d, skew, pool, seed = case
     layer = vc.case_layer(case)
@@ -50,7 +51,7 @@ def test_instance_against_oracle(sp, case):
     print("[case]", kind, variant, (N, C, K, H, W, R, S), "density", d, "skew", skew, flush=True)
     outs = {}
     ref = ab = None
-    for lowered in ((False, True) if kind == "s1" else (False,)):
+    for lowered in ((False, True) if kind != "dense" else (False,)):
         L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, 1, layer.pad, True, pool,
                                path="dense" if kind == "dense" else "sparse", lowered=lowered)
         plan = L.plan(N)
@@ -58,6 +59,8 @@ def test_instance_against_oracle(sp, case):
             (plan["pixels_per_lane"], plan["images_per_group"], plan["channels_per_wave"], int(pool))
         assert got == variant, (got, plan)
         assert (L.lowered(N) is not None) == lowered
+        if kind != "dense":  # the lowered "s1t" cases run several work items per workgroup
+            assert (plan["launch_workgroups"] < plan["workgroups"]) == (lowered and kind == "s1t"), plan
         print("[case]   lowered" if lowered else "[case]   plain", flush=True)
         out = L.run(torch.from_numpy(layer.x).cuda())
         torch.cuda.synchronize()

@@ -179,3 +179,25 @@ def test_forward_checks_the_stream(sp):
     assert fwd(0x10000, words.value + 1) == E     # size of another plan
     assert fwd(0x10004, words.value) == E         # not 16-byte aligned
     assert fwd(0x10000, words.value, stride=2) == E
+
+
+def _xcd_linear_id(b, G, xcds=8):
+    """Workgroup id -> XCD-ordered index, as the kernels compute it (common.h)."""
+    xcd, i = b % xcds, b // xcds
+    per, rem = G // xcds, G % xcds
+    return xcd * (per + 1) + i if xcd < rem else rem * (per + 1) + (xcd - rem) * per + i
+
+
+@pytest.mark.parametrize("T", [1, 7, 255, 256, 257, 300, 511, 512, 528, 3584, 4864, 4999])
+def test_persistent_schedule_takes_every_item_once(T):
+    """The lowered kernel's workgroup b of a grid of G = min(T, 256) takes, at
+    iteration t (while t*G + b < T), item t*G + its XCD-ordered index among
+    that round's min(G, T - t*G) items: every item exactly once."""
+    G = min(T, 256)
+    seen = []
+    for b in range(G):
+        t = 0
+        while t * G + b < T:
+            seen.append(t * G + _xcd_linear_id(b, min(G, T - t * G)))
+            t += 1
+    assert sorted(seen) == list(range(T))

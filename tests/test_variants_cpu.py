@@ -9,13 +9,15 @@ from paper_2005_04091_amd import spconv as sp
 
 
 def test_table_covers_every_compiled_instance():
-    s1 = set(sp.spconv_kernel_variants(sp.SPCONV_KERNEL_STRIDE1))
-    dense = set(sp.spconv_kernel_variants(sp.SPCONV_KERNEL_DENSE))
-    assert len(s1) == len(sp.spconv_kernel_variants(sp.SPCONV_KERNEL_STRIDE1))
-    have_s1 = {c[1] for c in vc.CASES if c[0] == "s1"}
-    have_dense = {c[1] for c in vc.CASES if c[0] == "dense"}
-    assert have_s1 == s1, f"missing {sorted(s1 - have_s1)}, stale {sorted(have_s1 - s1)}"
-    assert have_dense == dense, f"missing {sorted(dense - have_dense)}, stale {sorted(have_dense - dense)}"
+    for kind, family in (("s1", sp.SPCONV_KERNEL_STRIDE1), ("s1t", sp.SPCONV_KERNEL_STRIDE1_TILED),
+                         ("dense", sp.SPCONV_KERNEL_DENSE)):
+        compiled = sp.spconv_kernel_variants(family)
+        assert len(set(compiled)) == len(compiled)
+        have = {c[1] for c in vc.CASES if c[0] == kind}
+        assert have == set(compiled), f"{kind}: missing {sorted(set(compiled) - have)}, stale {sorted(have - set(compiled))}"
+    # the tiled form exists for a subset of the stride-1 tilings
+    assert set(sp.spconv_kernel_variants(sp.SPCONV_KERNEL_STRIDE1_TILED)) <= \
+        set(sp.spconv_kernel_variants(sp.SPCONV_KERNEL_STRIDE1))
     assert all(len(c) == 11 for c in vc.CASES), "a case without a shape"
 
 
@@ -26,7 +28,7 @@ def test_case_plans_to_its_instance(case):
 
 def test_cases_are_small():
     """Each case is a few hundred million multiply-adds of oracle work at most."""
-    assert max(vc.oracle_cost(c) for c in vc.CASES) < 3e8
+    assert max(vc.oracle_cost(c) for c in vc.CASES) < 4e8
     assert sum(vc.oracle_cost(c) for c in vc.CASES) < 3e9
 
 

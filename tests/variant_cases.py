@@ -23,13 +23,15 @@ if str(ROOT) not in sys.path:
     sys.path.insert(0, str(ROOT))
 
 # (kind, variant, N, C, K, H, W, density, skew, pool, seed); kind "s1" = stride-1
-# sparse kernel, variant (PI, IPW, RPW, pool); kind "dense", variant (R, S, NB, pool).
+# sparse kernel, variant (PI, IPW, RPW, pool); "s1t" = the same kernel run with
+# a lowered stream on more work items than one round of workgroups (the tiled
+# form); kind "dense", variant (R, S, NB, pool).
 CASES = [
     ('s1', (24, 1, 1, 0), 1, 3, 1040, 64, 64, 0.8, False, False, 5000),
     ('s1', (24, 1, 1, 1), 1, 3, 1040, 64, 64, 0.05, False, True, 5100),
     ('s1', (22, 1, 1, 0), 16, 3, 256, 36, 36, 0.8, False, False, 5200),
     ('s1', (22, 1, 1, 1), 2, 3, 1040, 36, 36, 0.05, False, True, 5300),
-    ('s1', (20, 1, 1, 0), 8, 3, 256, 48, 48, 0.8, False, False, 5400),
+    ('s1', (20, 1, 1, 0), 128, 3, 16, 48, 48, 0.05, False, False, 5400),
     ('s1', (20, 1, 1, 1), 1, 3, 1040, 56, 56, 0.05, False, True, 5500),
     ('s1', (18, 1, 1, 0), 64, 3, 16, 64, 64, 0.05, False, False, 5600),
     ('s1', (18, 1, 1, 1), 2, 3, 1040, 32, 32, 0.05, False, True, 5700),
@@ -37,11 +39,11 @@ CASES = [
     ('s1', (16, 1, 1, 1), 2, 3, 1040, 29, 29, 0.05, False, True, 5900),
     ('s1', (14, 1, 1, 0), 64, 3, 16, 56, 56, 0.05, True, False, 6000),
     ('s1', (14, 1, 1, 1), 2, 3, 1040, 27, 27, 0.05, False, True, 6100),
-    ('s1', (12, 1, 1, 0), 1, 3, 520, 64, 64, 0.8, False, False, 6200),
+    ('s1', (12, 1, 1, 0), 128, 3, 16, 36, 36, 0.05, True, False, 6200),
     ('s1', (12, 1, 1, 1), 2, 3, 1040, 25, 25, 0.05, False, True, 6300),
-    ('s1', (10, 1, 1, 0), 32, 3, 16, 64, 64, 0.05, True, False, 6400),
+    ('s1', (10, 1, 1, 0), 128, 3, 16, 31, 31, 0.05, True, False, 6400),
     ('s1', (10, 1, 1, 1), 2, 3, 1040, 22, 22, 0.05, False, True, 6500),
-    ('s1', (8, 1, 1, 0), 32, 3, 16, 56, 56, 0.05, True, False, 6600),
+    ('s1', (8, 1, 1, 0), 128, 3, 16, 27, 27, 0.05, True, False, 6600),
     ('s1', (8, 1, 1, 1), 2, 3, 1040, 19, 19, 0.05, False, True, 6700),
     ('s1', (6, 1, 1, 0), 64, 3, 16, 30, 30, 0.05, True, False, 6800),
     ('s1', (6, 1, 1, 1), 2, 3, 1040, 16, 16, 0.05, False, True, 6900),
@@ -51,7 +53,7 @@ CASES = [
     ('s1', (16, 1, 2, 1), 4, 3, 1040, 29, 29, 0.05, False, True, 7300),
     ('s1', (14, 1, 2, 0), 32, 3, 256, 27, 27, 0.2, False, False, 7400),
     ('s1', (14, 1, 2, 1), 4, 3, 1040, 27, 27, 0.05, False, True, 7500),
-    ('s1', (12, 1, 2, 0), 64, 3, 64, 64, 64, 0.05, True, False, 7602),
+    ('s1', (12, 1, 2, 0), 1, 3, 1040, 64, 64, 0.3, False, False, 7600),
     ('s1', (12, 1, 2, 1), 4, 3, 1040, 25, 25, 0.05, False, True, 7700),
     ('s1', (10, 1, 2, 0), 16, 3, 256, 31, 31, 0.2, False, False, 7800),
     ('s1', (10, 1, 2, 1), 4, 3, 1040, 22, 22, 0.05, False, True, 7900),
@@ -99,44 +101,64 @@ CASES = [
     ('s1', (2, 4, 2, 1), 16, 3, 1040, 2, 2, 0.05, False, True, 12100),
     ('s1', (2, 4, 4, 0), 32, 3, 1040, 2, 2, 0.05, False, False, 12200),
     ('s1', (2, 4, 4, 1), 32, 3, 1040, 2, 2, 0.2, True, True, 12300),
-    ('dense', (3, 3, 1, 0), 1, 3, 16, 2, 2, 0.3, False, False, 12400),
-    ('dense', (3, 3, 1, 1), 1, 3, 16, 2, 2, 0.3, False, True, 12500),
-    ('dense', (3, 3, 2, 0), 1, 3, 16, 31, 31, 0.3, False, False, 12600),
-    ('dense', (3, 3, 2, 1), 1, 3, 16, 15, 15, 0.3, False, True, 12700),
-    ('dense', (3, 3, 3, 0), 1, 3, 16, 64, 64, 0.3, False, False, 12800),
-    ('dense', (3, 3, 3, 1), 1, 3, 16, 31, 31, 0.3, False, True, 12900),
-    ('dense', (3, 3, 4, 0), 1, 3, 16, 112, 112, 0.3, False, False, 13000),
-    ('dense', (3, 3, 4, 1), 1, 3, 16, 48, 48, 0.3, False, True, 13100),
-    ('dense', (3, 3, 5, 0), 32, 3, 16, 64, 64, 0.3, False, False, 13200),
-    ('dense', (3, 3, 5, 1), 1, 3, 16, 64, 64, 0.3, False, True, 13300),
-    ('dense', (3, 3, 6, 0), 2, 3, 520, 80, 80, 0.3, False, False, 13400),
-    ('dense', (3, 3, 6, 1), 1, 3, 16, 80, 80, 0.3, False, True, 13500),
-    ('dense', (3, 3, 7, 0), 64, 3, 16, 64, 64, 0.3, False, False, 13600),
-    ('dense', (3, 3, 7, 1), 64, 3, 16, 48, 48, 0.3, False, True, 13700),
-    ('dense', (3, 3, 8, 0), 1, 3, 16, 224, 224, 0.3, False, False, 13800),
-    ('dense', (3, 3, 8, 1), 1, 3, 16, 112, 112, 0.3, False, True, 13900),
-    ('dense', (1, 1, 1, 0), 1, 3, 16, 2, 2, 0.3, False, False, 14000),
-    ('dense', (1, 1, 1, 1), 1, 3, 16, 2, 2, 0.3, False, True, 14100),
-    ('dense', (1, 1, 2, 0), 1, 3, 16, 36, 36, 0.3, False, False, 14200),
-    ('dense', (1, 1, 2, 1), 1, 3, 16, 17, 17, 0.3, False, True, 14300),
-    ('dense', (1, 1, 3, 0), 1, 3, 16, 80, 80, 0.3, False, False, 14400),
-    ('dense', (1, 1, 3, 1), 1, 3, 16, 36, 36, 0.3, False, True, 14500),
-    ('dense', (1, 1, 4, 0), 1, 3, 16, 112, 112, 0.3, False, False, 14600),
-    ('dense', (1, 1, 4, 1), 1, 3, 16, 56, 56, 0.3, False, True, 14700),
-    ('dense', (1, 1, 5, 0), 32, 3, 16, 80, 80, 0.3, False, False, 14800),
-    ('dense', (1, 1, 5, 1), 1, 3, 16, 80, 80, 0.3, False, True, 14900),
-    ('dense', (1, 1, 6, 0), 64, 3, 16, 48, 48, 0.3, False, False, 15000),
-    ('dense', (1, 1, 6, 1), 64, 3, 16, 48, 48, 0.3, False, True, 15100),
-    ('dense', (1, 1, 7, 0), 1, 3, 16, 224, 224, 0.3, False, False, 15200),
-    ('dense', (1, 1, 7, 1), 1, 3, 16, 112, 112, 0.3, False, True, 15300),
-    ('dense', (1, 1, 8, 0), 64, 3, 16, 64, 64, 0.3, False, False, 15400),
-    ('dense', (1, 1, 8, 1), 64, 3, 16, 64, 64, 0.3, False, True, 15500),
+    ('s1t', (24, 1, 1, 0), 16, 3, 256, 64, 64, 0.8, False, False, 12400),
+    ('s1t', (24, 1, 1, 1), 2, 3, 1040, 64, 64, 0.05, False, True, 12500),
+    ('s1t', (22, 1, 1, 0), 32, 3, 256, 36, 36, 0.8, False, False, 12600),
+    ('s1t', (22, 1, 1, 1), 4, 3, 1040, 36, 36, 0.05, False, True, 12700),
+    ('s1t', (20, 1, 1, 0), 16, 3, 256, 48, 48, 0.8, False, False, 12800),
+    ('s1t', (20, 1, 1, 1), 2, 3, 1040, 56, 56, 0.05, False, True, 12900),
+    ('s1t', (18, 1, 1, 0), 128, 3, 16, 64, 64, 0.05, False, False, 13000),
+    ('s1t', (18, 1, 1, 1), 4, 3, 1040, 32, 32, 0.05, False, True, 13100),
+    ('s1t', (16, 1, 1, 0), 8, 3, 16, 224, 224, 0.05, True, False, 13200),
+    ('s1t', (16, 1, 1, 1), 32, 3, 16, 112, 112, 0.05, False, True, 13300),
+    ('s1t', (14, 1, 1, 0), 128, 3, 16, 56, 56, 0.05, True, False, 13400),
+    ('s1t', (14, 1, 1, 1), 8, 3, 1040, 27, 27, 0.05, False, True, 13500),
+    ('s1t', (12, 1, 1, 0), 16, 3, 1040, 25, 25, 0.8, False, False, 13600),
+    ('s1t', (12, 1, 1, 1), 8, 3, 1040, 25, 25, 0.05, False, True, 13700),
+    ('s1t', (16, 1, 2, 0), 8, 3, 16, 224, 224, 0.05, False, False, 13806),
+    ('s1t', (16, 1, 2, 1), 64, 3, 256, 29, 29, 0.05, False, True, 13900),
+    ('s1t', (14, 1, 2, 0), 64, 3, 256, 27, 27, 0.2, False, False, 14000),
+    ('s1t', (14, 1, 2, 1), 64, 3, 256, 27, 27, 0.05, False, True, 14100),
+    ('s1t', (12, 1, 2, 0), 16, 3, 256, 64, 64, 0.05, True, False, 14200),
+    ('s1t', (12, 1, 2, 1), 64, 3, 256, 25, 25, 0.05, False, True, 14300),
+    ('dense', (3, 3, 1, 0), 1, 3, 16, 2, 2, 0.3, False, False, 14400),
+    ('dense', (3, 3, 1, 1), 1, 3, 16, 2, 2, 0.3, False, True, 14500),
+    ('dense', (3, 3, 2, 0), 1, 3, 16, 31, 31, 0.3, False, False, 14600),
+    ('dense', (3, 3, 2, 1), 1, 3, 16, 15, 15, 0.3, False, True, 14700),
+    ('dense', (3, 3, 3, 0), 1, 3, 16, 64, 64, 0.3, False, False, 14800),
+    ('dense', (3, 3, 3, 1), 1, 3, 16, 31, 31, 0.3, False, True, 14900),
+    ('dense', (3, 3, 4, 0), 1, 3, 16, 112, 112, 0.3, False, False, 15000),
+    ('dense', (3, 3, 4, 1), 1, 3, 16, 48, 48, 0.3, False, True, 15100),
+    ('dense', (3, 3, 5, 0), 128, 3, 16, 29, 29, 0.3, False, False, 15200),
+    ('dense', (3, 3, 5, 1), 1, 3, 16, 64, 64, 0.3, False, True, 15300),
+    ('dense', (3, 3, 6, 0), 128, 3, 64, 21, 21, 0.3, False, False, 15400),
+    ('dense', (3, 3, 6, 1), 1, 3, 16, 80, 80, 0.3, False, True, 15500),
+    ('dense', (3, 3, 7, 0), 64, 3, 16, 64, 64, 0.3, False, False, 15600),
+    ('dense', (3, 3, 7, 1), 64, 3, 16, 48, 48, 0.3, False, True, 15700),
+    ('dense', (3, 3, 8, 0), 1, 3, 16, 224, 224, 0.3, False, False, 15800),
+    ('dense', (3, 3, 8, 1), 1, 3, 16, 112, 112, 0.3, False, True, 15900),
+    ('dense', (1, 1, 1, 0), 1, 3, 16, 2, 2, 0.3, False, False, 16000),
+    ('dense', (1, 1, 1, 1), 1, 3, 16, 2, 2, 0.3, False, True, 16100),
+    ('dense', (1, 1, 2, 0), 1, 3, 16, 36, 36, 0.3, False, False, 16200),
+    ('dense', (1, 1, 2, 1), 1, 3, 16, 17, 17, 0.3, False, True, 16300),
+    ('dense', (1, 1, 3, 0), 1, 3, 16, 80, 80, 0.3, False, False, 16400),
+    ('dense', (1, 1, 3, 1), 1, 3, 16, 36, 36, 0.3, False, True, 16500),
+    ('dense', (1, 1, 4, 0), 1, 3, 16, 112, 112, 0.3, False, False, 16600),
+    ('dense', (1, 1, 4, 1), 1, 3, 16, 56, 56, 0.3, False, True, 16700),
+    ('dense', (1, 1, 5, 0), 128, 3, 16, 29, 29, 0.3, False, False, 16800),
+    ('dense', (1, 1, 5, 1), 1, 3, 16, 80, 80, 0.3, False, True, 16900),
+    ('dense', (1, 1, 6, 0), 64, 3, 16, 48, 48, 0.3, False, False, 17000),
+    ('dense', (1, 1, 6, 1), 64, 3, 16, 48, 48, 0.3, False, True, 17100),
+    ('dense', (1, 1, 7, 0), 1, 3, 16, 224, 224, 0.3, False, False, 17200),
+    ('dense', (1, 1, 7, 1), 1, 3, 16, 112, 112, 0.3, False, True, 17300),
+    ('dense', (1, 1, 8, 0), 64, 3, 16, 64, 64, 0.3, False, False, 17400),
+    ('dense', (1, 1, 8, 1), 64, 3, 16, 64, 64, 0.3, False, True, 17500),
 ]
 
 # Shapes the search tries (small enough that the oracle finishes in well under
 # a second per case at the chosen one).
 _SEARCH_H = list(range(2, 33)) + [36, 40, 48, 56, 64, 80, 112, 224]
-_SEARCH_N = (1, 2, 4, 8, 16, 32, 64)
+_SEARCH_N = (1, 2, 4, 8, 16, 32, 64, 128)
 _SEARCH_C = (3, 16, 32, 64, 250)
 _SEARCH_K = (16, 64, 128, 256, 520, 1040)
 
@@ -163,11 +185,13 @@ def planned_variant(case, layer=None):
         p = sp.spconv_dense_plan(N, C, H, W, K, R, S, layer.pad, flags)
         return (R, S, p["pixels_per_lane"], int(pool))
     host = sp.spconv_pack_csr(layer.w, layer.mask, H + 2 * layer.pad, W + 2 * layer.pad)
-    st = sp.spconv_csr(K, C, R, S, host.Hp, host.Wp, host.nnz, host.rowptr.ctypes.data, host.colidx.ctypes.data,
-                       host.offset.ctypes.data, host.vals.ctypes.data)
     mx = int(np.diff(host.rowptr).max())
-    p = sp.spconv_plan(N, C, H, W, st, K, R, S, 1, layer.pad, flags, max_row_nnz=mx)
+    p = sp.spconv_plan(N, C, H, W, sp.host_csr_struct(host), K, R, S, 1, layer.pad, flags, max_row_nnz=mx,
+                       lowered=True)
     if p["kernel"] != sp.SPCONV_KERNEL_STRIDE1:
+        return None
+    # "s1t": the lowered launch runs several work items per workgroup
+    if (kind == "s1t") != (p["launch_workgroups"] < p["workgroups"]):
         return None
     return (p["pixels_per_lane"], p["images_per_group"], p["channels_per_wave"], int(pool))
 
@@ -185,6 +209,7 @@ def search():
     from paper_2005_04091_amd import spconv as sp
     dummy = np.zeros(4, np.int32)
     ptr = dummy.ctypes.data
+    tiled = set(sp.spconv_kernel_variants(sp.SPCONV_KERNEL_STRIDE1_TILED))
     cands = {}
     for H in _SEARCH_H:
         for N in _SEARCH_N:
@@ -209,7 +234,8 @@ def search():
                                 if p["kernel"] != sp.SPCONV_KERNEL_STRIDE1:
                                     continue
                                 v = (p["pixels_per_lane"], p["images_per_group"], p["channels_per_wave"], int(pool))
-                                cands.setdefault(v, []).append(("s1", v, N, C, K, H, H, d, skew, pool, 0))
+                                kind = "s1t" if p["workgroups"] > 256 and v in tiled else "s1"
+                                cands.setdefault((kind, v), []).append((kind, v, N, C, K, H, H, d, skew, pool, 0))
                         for rs in (3, 1):
                             try:
                                 p = sp.spconv_dense_plan(N, C, H, H, K, rs, rs, (rs - 1) // 2,
@@ -217,18 +243,20 @@ def search():
                             except sp.SpconvError:
                                 continue
                             v = (rs, rs, p["pixels_per_lane"], int(pool))
-                            cands.setdefault(v, []).append(("dense", v, N, C, K, H, H, 0.3, False, pool, 0))
+                            cands.setdefault(("dense", v), []).append(("dense", v, N, C, K, H, H, 0.3, False, pool, 0))
     table = []
     wanted = [("s1", v) for v in sp.spconv_kernel_variants(sp.SPCONV_KERNEL_STRIDE1)] + \
+             [("s1t", v) for v in sp.spconv_kernel_variants(sp.SPCONV_KERNEL_STRIDE1_TILED)] + \
              [("dense", v) for v in sp.spconv_kernel_variants(sp.SPCONV_KERNEL_DENSE)]
     for kind, v in wanted:
         got = None
-        for c in sorted(cands.get(v, []), key=oracle_cost):
+        pool_of = cands.get((kind, v), []) + (cands.get(("s1t", v), []) if kind == "s1" else [])
+        for c in sorted(pool_of, key=oracle_cost):
             _, _, N, C, K, H, W = c[:7]
             if N * C * H * W > 4_000_000 or K * C * 9 > 4_000_000:
                 continue  # too large to draw for a test case
             for seed in range(5000 + 100 * len(table), 5000 + 100 * len(table) + 8):
-                case = c[:-1] + (seed,)
+                case = (kind,) + c[1:-1] + (seed,)
                 if planned_variant(case) == v:
                     got = case
                     break
