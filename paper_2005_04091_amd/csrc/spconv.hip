@@ -442,6 +442,9 @@ struct FwdArgs {
     // (LDS index, weight) pairs and an over-read pad of kLwPad pairs
     int lw_headers;
     int lw_entries;
+    // pooled epilogue: the pitch vp is even, so pixel pairs are horizontal
+    // pool pairs (pair-maxima staging), and that staging fits one chunk buffer
+    int pool_pairs, pool_in_buf;
 };
 
 // Entries fetched per scalar load in the lowered walk (one s_load_dwordx16),
@@ -918,11 +921,19 @@ constexpr int lowered_pipeline_buffers() {
 // the wave's RPW channels krow over the tile (images ig*IPW.., rows y0..).
 // The pooled form reuses the chunk buffers: every wave must be past its last
 // read of them (a barrier) before the call.
+//
+// Pooled staging: with an even tile pitch (a.pool_pairs) a lane's pixel pair
+// (2l, 2l+1) + 128j is one horizontal pool pair, so each wave stages only
+// the pair maxima (64 * PI/2 floats per image) at `stage`, and a pooled output
+// takes the larger of two staged maxima one pitch apart (the same maxima as
+// over the four pixels, same bits). Otherwise whole activated tiles are staged
+// from `lds` on, over both chunk buffers.
 template <int PI, int IPW, int RPW, bool POOL>
 __device__ __forceinline__ void s1_epilogue(const FwdArgs &a, float2 (&accE)[RPW][IPW][PI / 2],
                                             float2 (&accO)[RPW][IPW][PI / 2], const int (&krow)[RPW], int ig, int ty,
-                                            int y0, int wave, int lane, float *lds, const float *__restrict__ bias,
-                                            const float *__restrict__ res, float *__restrict__ out) {
+                                            int y0, int wave, int lane, float *lds, float *stage,
+                                            const float *__restrict__ bias, const float *__restrict__ res,
+                                            float *__restrict__ out) {
     constexpr int PJ = PI / 2;
     const int q = 2 * lane;
     const int tile_px = a.TH * a.vp;
@@ -991,6 +1002,73 @@ __device__ __forceinline__ void s1_epilogue(const FwdArgs &a, float2 (&accE)[RPW
                 if (a.out_pad)
                     zero_border(plane, y0, min(y0 + a.TH, a.Ho), a.Ho, a.Wo, a.out_pad, a.opitch, ty == 0,
                                 ty == a.ntiles_y - 1, lane, kWave);
+            }
+        }
+    } else if (a.pool_pairs) {
+        // Pair maxima, staged per wave (see above); only the wave's own LDS
+        // order matters, and the last barrier of the chunk loop ordered these
+        // writes after every wave's reads of the staging buffer.
+        constexpr int kImgPairs = kWave * PJ;
+        float *st = stage + wave * IPW * kImgPairs;
+        const int prow0 = y0 / 2;
+        const int prows = a.TH / 2;
+        const int per_img = prows * a.Wq;
+        const int half = a.vp / 2;
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+            const int k = krow[i];
+            const float bk = (k < a.K && bias) ? bias[k] : 0.0f;
+#pragma unroll
+            for (int im = 0; im < IPW; ++im) {
+                float2 sum[PJ];
+                merge_pairs(accE[i][im], accO[i][im], sum, lane);
+                const int n = ig * IPW + im;
+                const float *rp = (res && k < a.K && n < a.N)
+                                      ? res + ((size_t)n * a.K + k) * a.rplane +
+                                            (size_t)(y0 + a.res_pad) * a.rpitch + a.res_pad
+                                      : nullptr;
+#pragma unroll
+                for (int p = 0; p < PJ; ++p) {
+                    float v[2] = {sum[p].x + bk, sum[p].y + bk};
+                    if (rp) {
+#pragma unroll
+                        for (int h = 0; h < 2; ++h) {
+                            const int qq = q + 2 * kWave * p + h;
+                            const int yl = (int)fast_div((uint32_t)qq, a.vp_magic, a.vp_shift), x = qq - yl * a.vp;
+                            if (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) v[h] += rp[qq + yl * (a.rpitch - a.vp)];
+                        }
+                    }
+                    if (a.relu) {
+                        v[0] = v[0] > 0.0f ? v[0] : 0.0f;
+                        v[1] = v[1] > 0.0f ? v[1] : 0.0f;
+                    }
+                    st[im * kImgPairs + lane + kWave * p] = fmaxf(v[0], v[1]);
+                }
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // the pair maxima are staged
+            if (k < a.K) {
+                for (int t = lane; t < IPW * per_img; t += kWave) {
+                    const int im = (int)fast_div((uint32_t)t, a.pimg_magic, a.pimg_shift);
+                    const int rem = t - im * per_img;
+                    const int r = (int)fast_div((uint32_t)rem, a.wq_magic, a.wq_shift);
+                    const int jq = rem - r * a.Wq;
+                    const int n = ig * IPW + im;
+                    const int pr = prow0 + r;
+                    if (n < a.N && pr < a.Hq) {
+                        const float *s0 = st + im * kImgPairs + r * a.vp + jq;
+                        const float m = fmaxf(s0[0], s0[half]);
+                        store_out(out + ((size_t)n * a.K + k) * a.oplane + (size_t)(pr + a.out_pad) * a.opitch + jq +
+                                      a.out_pad,
+                                  m, a.out_pad == 0);
+                    }
+                }
+                if (a.out_pad)
+                    for (int im = 0; im < IPW; ++im) {
+                        const int n = ig * IPW + im;
+                        if (n >= a.N) break;
+                        zero_border(out + ((size_t)n * a.K + k) * a.oplane, prow0, min(prow0 + prows, a.Hq), a.Hq,
+                                    a.Wq, a.out_pad, a.opitch, ty == 0, ty == a.ntiles_y - 1, lane, kWave);
+                    }
             }
         }
     } else {
@@ -1147,7 +1225,7 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
             float *nbuf = lds + (sbuf ^ 1) * a.buf_floats;
             if (more)
                 stage_chunk_s1(a, xp, nbuf, ch + 1, cur.ig, y0, wave, lane, PERSIST);
-            else if (!POOL && has_next)
+            else if ((!POOL || a.pool_in_buf) && has_next)
                 stage_chunk_s1(a, xp, nbuf, 0, nxt.ig, nxt.ty * a.TH, wave, lane, PERSIST);
             // Entry lists of this chunk, clamped to the stream.
             int st[RPW], ne[RPW], no[RPW];
@@ -1183,9 +1261,18 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
             }
             sbuf ^= 1;
         }
-        s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, cur.ig, cur.ty, y0, wave, lane, lds, bias, res, out);
+        // The pooled staging goes to the buffer of the last chunk (now free)
+        // when it fits there, else over both buffers.
+        float *stage = (POOL && a.pool_in_buf) ? lds + (sbuf ^ 1) * a.buf_floats : lds;
+        s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, cur.ig, cur.ty, y0, wave, lane, lds, stage, bias, res,
+                                        out);
         if (!has_next) break;
-        if constexpr (POOL) {
+        if (POOL && a.pool_in_buf) {
+            // The next tile's first chunk is in the other buffer; its second
+            // chunk's copy into the staging buffer waits for every wave's
+            // pooled reads.
+            __syncthreads();
+        } else if constexpr (POOL) {
             // The staging tile overlaps the buffers: the next tile's first
             // chunk is copied after every wave's pooled stores. With an
             // unpadded input the staging also overwrote border positions that
@@ -1366,7 +1453,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
         }
     }
 
-    s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, ig, ty, y0, wave, lane, lds, bias, res, out);
+    s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, ig, ty, y0, wave, lane, lds, lds, bias, res, out);
 }
 
 // Generic-stride kernel: waves split the pixels of the tile and every wave
@@ -2017,6 +2104,7 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.dma16 = row16 ? 1 : 0;
     a.pair_store = 0;
     a.lw_headers = a.lw_entries = 0;
+    a.pool_pairs = a.pool_in_buf = 0;
     if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift)) return SPCONV_EINVAL;
     if (!div_magic((uint32_t)a.vp, &a.vp_magic, &a.vp_shift)) return SPCONV_EINVAL;
     a.H = H;
@@ -2051,6 +2139,17 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.PL = pl.PL;
     a.img_lds = pl.img_lds;
     a.buf_floats = pl.buf_floats;
+    if (pl.kind == Kind::kStride1 && pool) {
+        // Pair-maxima staging needs an even pitch; it fits the buffer of the
+        // last chunk when 16 waves x IPW images x 64 lanes x PI/2 maxima do
+        // (and the input is padded: an unpadded input's buffers keep border
+        // zeros that no copy rewrites, which the staging would overwrite).
+        a.pool_pairs = (a.vp % 2 == 0) ? 1 : 0;
+        a.pool_in_buf = (a.pool_pairs && !unpadded &&
+                         (long long)kS1Waves * pl.IPW * kWave * (pl.PI / 2) <= (long long)pl.buf_floats)
+                            ? 1
+                            : 0;
+    }
     a.PLp = pl.PLp;
     a.total_floats = (size_t)N * C * Hp * Wp;
     a.wv = pl.wv;

@@ -263,6 +263,9 @@ VARIANTS = [
     # lowered kernel runs several work items per workgroup
     ("ipw1_rpw1_495_items", 33, 3, 48, 64, False, False, (14, 1, 1)),
     ("ipw1_rpw1_pool_495_items", 33, 3, 48, 56, True, False, (12, 1, 1)),
+    # ... with the pooled staging of pair maxima in the last chunk's buffer,
+    # so the next tile's first chunk is copied during the last one (504 items)
+    ("ipw1_rpw1_pool_pairs_504_items", 9, 32, 16, 224, True, False, (16, 1, 1)),
 ]
 
 
