@@ -425,7 +425,7 @@ def bench_resize_block(args, dev):
 
 METRIC = "ms/layer + nonzero GFLOP/s + % HBM roofline, fused sparse conv, 1 MI355X"
 DATA = "synthetic (seeded Bernoulli-masked weights U[-1,1), input U[0,1), bias U[-0.1,0.1))"
-COLD_REPS = 30  # the paper reports the median of 30 runs
+COLD_REPS = 30  # the paper reports the median of 30 runs (--cold-reps changes it for profiling runs)
 
 
 def layer_launch(L, x, out, stream, xp=None):
@@ -464,8 +464,8 @@ def per_config_record(name, args, dev, stream):
         fwd()
 
     ms_warm = _timed(args, stream, fwd)
-    ms_cold = cold_median_ms(fwd, stream, COLD_REPS, dev)
-    ms_step_cold = cold_median_ms(step, stream, COLD_REPS, dev)
+    ms_cold = cold_median_ms(fwd, stream, args.cold_reps, dev)
+    ms_step_cold = cold_median_ms(step, stream, args.cold_reps, dev)
     nnz = L.host_csr.nnz
     flops, nbytes, _ = algorithmic(layer, nnz)
     if fused_pad:
@@ -610,8 +610,8 @@ def bench_vgg(args, dev):
     ms2 = statistics.mean(e[1].elapsed_time(e[2]) for e in ev)
     print(f"[bench] step {ms_per_step:.4f} ms, conv1 {ms1:.4f} ms, conv2+pool {ms2:.4f} ms", file=sys.stderr,
           flush=True)
-    cold1 = cold_median_ms(conv1, stream, COLD_REPS, dev)
-    cold2 = cold_median_ms(conv2, stream, COLD_REPS, dev)
+    cold1 = cold_median_ms(conv1, stream, args.cold_reps, dev)
+    cold2 = cold_median_ms(conv2, stream, args.cold_reps, dev)
     copy_gbs = measured_copy_gbs(dev)
 
     nnz1, nnz2 = L1.host_csr.nnz, L2.host_csr.nnz
@@ -653,7 +653,7 @@ def bench_vgg(args, dev):
         "config": {"workload": BLOCKS["vgg_block"], "N": N, "C": C, "K": K, "H": H, "W": W, "R": R, "S": S,
                    "nnz": [nnz1, nnz2], "density": 0.2, "pool": "layer 2", "path": "sparse"},
         "ms_per_layer": {k: v["ms_per_layer"] for k, v in layers.items()},
-        "ms_per_layer_protocol": f"median of {COLD_REPS} runs, each after a 512 MiB write that flushes the "
+        "ms_per_layer_protocol": f"median of {args.cold_reps} runs, each after a 512 MiB write that flushes the "
                                  "last-level cache; HIP events around the forward alone",
         "layers": layers,
         "hbm_copy_measured_GBs": round(copy_gbs, 1),
@@ -688,6 +688,8 @@ def bench_vgg(args, dev):
         rec["per_config"] = pc
         rec["hbm_bar"]["max_hbm_frac_at_fma_peak"].update(
             {r["workload"]: r["roof"]["max_hbm_frac_at_compute_peak"] for r in pc})
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, dev)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on the block", file=sys.stderr, flush=True)
         rec["cpu_baseline"] = cpu_baseline_block([l1, l2], args.cpu_budget)
@@ -704,6 +706,8 @@ def main():
                          "its fused and unfused variants instead; other names: one layer or block")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-reps", type=int, default=COLD_REPS,
+                    help="runs per cache-flushed median (30, as the paper's medians; fewer for counter runs)")
     ap.add_argument("--no-per-config", action="store_true",
                     help="default workload only: leave out the per-config records of the other layers")
     ap.add_argument("--cold", action="store_true",

@@ -247,7 +247,7 @@ int spconv_forward_ex(const float *in_padded, int N, int C, int H, int W, const 
  * the slot's first entry of that chunk), followed by every CSR entry once as
  * an int32 pair (LDS index of the pixel pair the tap reads for virtual pixel 0
  * of the chunk, the value's bits), the even-parity taps of a (slot, chunk)
- * before its odd ones, each in CSR order; then 8 zero pairs of padding. With
+ * before its odd ones, each in CSR order; then 16 zero pairs of padding. With
  * the plan's spconv_plan_info, entry (c, r, s) of the chunk starting at
  * channel c0 = chunk * channels_per_chunk has LDS index t = (c - c0) *
  * lds_channel_floats + r * lds_row_pitch + s + lds_col_shift; its parity is
@@ -261,7 +261,7 @@ int spconv_forward_ex(const float *in_padded, int N, int C, int H, int W, const 
 /*
  * spconv_lowered_size - int32 words of the lowered stream for a forward call
  * with these arguments (host only; csr's arrays are not read):
- *   4 * tiles * 16 * channels_per_wave * chunks + 2 * (nnz + 8).
+ *   4 * tiles * 16 * channels_per_wave * chunks + 2 * (nnz + 16).
  * Errors: those of spconv_forward_ex's argument checks (opt->lowered is not
  * looked at); SPCONV_EINVAL for a NULL words or a plan other than the
  * stride-1 kernel.

@@ -448,9 +448,10 @@ struct FwdArgs {
 };
 
 // Entries fetched per scalar load in the lowered walk (one s_load_dwordx16),
-// and the pad of entries after the stream that such loads may read.
+// and the pad of entries after the stream that such loads may read (a walk
+// near the end of the stream loads the batch after its current one).
 constexpr int kLwBatch = 8;
-constexpr int kLwPad = kLwBatch;
+constexpr int kLwPad = 2 * kLwBatch;
 
 // Queue asynchronous global->LDS copies of one channel chunk: for each image of
 // the group and each channel of the chunk, seg_len consecutive floats (the
@@ -807,9 +808,21 @@ __device__ __forceinline__ void run_range(float2 (&acc)[IPW][PJ], int lo, float 
 // load each, so index and weight are wave-uniform SGPRs: an entry costs one
 // address add and its FMAs (the weight is the FMAs' scalar operand), no
 // broadcast. Software pipeline of NB pixel-pair buffers as in run_range; the
-// next batch is loaded NB entries before its first use, so its scalar load
+// next batch is loaded one entry before its first use, so its scalar load
 // overlaps one entry's FMAs (scalar loads complete out of order with LDS
-// reads, so the first LDS wait after it waits for both).
+// reads, so the first LDS wait after it waits for both). The main loop's body
+// has no branch (a branch would let the compiler move every FMA of the batch
+// behind its reads, with register copies between); list ends are handled in a
+// guarded tail.
+// Calls f(integral_constant<int, U>) for U = I, I+1, ... below END while it
+// returns true: a loop unrolled at compile time, with a constant index.
+template <int I, int END, typename F>
+__device__ __forceinline__ void unroll_while(F &&f) {
+    if constexpr (I < END) {
+        if (f(std::integral_constant<int, I>{})) unroll_while<I + 1, END>(f);
+    }
+}
+
 template <int B>
 struct LwBatch {
     int v[2 * B];
@@ -827,34 +840,48 @@ __device__ __forceinline__ void run_lowered(float2 (&acc)[IPW][PJ], const int32_
     for (int u = 0; u < NB - 1; ++u)
         if (u < n) load_pairs(x[u], lds, b.v[2 * u] + qv, img_lds);
     int r = n;
-    // Full batches followed by at least one more entry: the loads of entry
-    // u + NB - 1 may come from the next batch.
-    for (; r > B; r -= B) {
+    // Main loop, branch free: a whole batch, and the NB - 1 entries whose
+    // reads issue ahead of it all exist (the first of them come from the
+    // next batch).
+    for (; r >= B + NB - 1; r -= B) {
         LwBatch<B> nb;
 #pragma unroll
         for (int u = 0; u < B; ++u) {
             if (u == B - NB) nb = *reinterpret_cast<const LwBatch<B> *>(ent + 2 * (j + B));
-            const int f = u + NB - 1;  // entry whose loads issue now
-            if (f < B) {
-                load_pairs(x[f % NB], lds, b.v[2 * f] + qv, img_lds);
-            } else if (f - B < r - B) {
-                load_pairs(x[f % NB], lds, nb.v[2 * (f - B)] + qv, img_lds);
-            }
+            const int f = u + NB - 1;  // entry whose reads issue now
+            load_pairs(x[f % NB], lds, (f < B ? b.v[2 * f] : nb.v[2 * (f - B)]) + qv, img_lds);
             fma_pairs(acc, x[u % NB], __int_as_float(b.v[2 * u + 1]));
             __builtin_amdgcn_sched_barrier(0);
         }
         b = nb;
         j += B;
     }
-    // Last batch: r entries (1..B); entries below NB - 1 are in flight.
-#pragma unroll
-    for (int u = 0; u < B; ++u) {
-        if (u >= r) break;
-        const int f = u + NB - 1;
-        if (f < r) load_pairs(x[f % NB], lds, b.v[2 * f] + qv, img_lds);
-        fma_pairs(acc, x[u % NB], __int_as_float(b.v[2 * u + 1]));
+    // Tail: r < B + NB - 1 entries, the first min(r, NB - 1) in flight; past
+    // entry B - 1 they come from the next batch. That batch is loaded
+    // whether or not the list reaches it (a conditional load would not stay
+    // scalar); the stream's pad of two batches keeps it inside the stream.
+    const LwBatch<B> nb = *reinterpret_cast<const LwBatch<B> *>(ent + 2 * (j + B));
+    // Unrolled at compile time (a loop with this early exit is not), so every
+    // batch index is a constant and the batches stay in SGPRs.
+    unroll_while<0, B + NB - 1>([&](auto U) {
+        constexpr int u = decltype(U)::value;
+        constexpr int f = u + NB - 1;
+        if (u >= r) return false;
+        if (f < r) {
+            if constexpr (f < B)
+                load_pairs(x[f % NB], lds, b.v[2 * f] + qv, img_lds);
+            else
+                load_pairs(x[f % NB], lds, nb.v[2 * (f - B)] + qv, img_lds);
+        }
+        float w;
+        if constexpr (u < B)
+            w = __int_as_float(b.v[2 * u + 1]);
+        else
+            w = __int_as_float(nb.v[2 * (u - B) + 1]);
+        fma_pairs(acc, x[u % NB], w);
         __builtin_amdgcn_sched_barrier(0);
-    }
+        return true;
+    });
 }
 
 // Pipeline depth of the stride-1 kernel: deeper for fewer FMAs per entry

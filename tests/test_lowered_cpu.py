@@ -58,7 +58,7 @@ def reference_stream(host, plan, K, C, R, S):
                                 counts[parity] += 1
                     headers.append((start, counts[0], counts[1], min(k, K)))
     out = np.array(headers, np.int32).reshape(-1)
-    ent = np.array(entries + [(0, 0)] * 8, np.int32).reshape(-1)
+    ent = np.array(entries + [(0, 0)] * 16, np.int32).reshape(-1)
     return np.concatenate([out, ent])
 
 
@@ -90,7 +90,7 @@ def test_stream_matches_documented_layout(sp, case):
     assert got.shape == ref.shape
     assert np.array_equal(got, ref)
     nh = -(-K // (16 * plan["channels_per_wave"])) * 16 * plan["channels_per_wave"] * plan["chunks"]
-    assert got.size == 4 * nh + 2 * (host.nnz + 8)
+    assert got.size == 4 * nh + 2 * (host.nnz + 16)
 
 
 def test_stream_plans_cover_the_interesting_tilings(sp):
