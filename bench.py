@@ -420,6 +420,8 @@ def bench_resize_block(args, dev):
                           "GB/s": round(rbytes / (ms_resize * 1e-3) / 1e9, 1),
                           "hbm_frac": round(rbytes / (ms_resize * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
     }
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, dev)
     print(json.dumps(rec), flush=True)
 
 

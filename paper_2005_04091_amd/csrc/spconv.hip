@@ -422,12 +422,14 @@ struct FwdArgs {
     int unpadded;
     int H, W, pad;
     // stride-1 kernel: pitch of the virtual tile and of the staged LDS rows
-    // (Wp, or Wp rounded up to 4 for 16-byte row copies of an unpadded input),
-    // the LDS column of padded column 0 (lds_shift), and whether rows are
-    // copied 16 bytes per lane
+    // (Wp, or Wp rounded up to 4 when an unpadded input's rows are whole
+    // 16-byte groups), the LDS column of padded column 0 (lds_shift), and
+    // whether an unpadded input is copied 16 bytes per lane
     int vp, lds_shift, dma16;
     uint32_t wp_magic;  // x / Wp == (x * wp_magic) >> wp_shift
     int wp_shift;
+    uint32_t plp_magic;  // x / PLp (stride-1 kernel's unpadded staging)
+    int plp_shift;
     // stride-1 epilogues: x / vp, x / ((TH/2) * Wq) and x / Wq as multiply-
     // shift (a runtime integer division is some 30 instructions, several of
     // them quarter rate, per stored pixel)
@@ -488,73 +490,66 @@ constexpr int kS1LdsFloats = 40960;  // 160 KiB: one workgroup per CU, two chunk
 constexpr int kStageBlock = 256;     // floats per 16-byte-per-lane LDS DMA instruction
 
 // Queue the asynchronous copy of one channel chunk: for each image of the group
-// and each channel of the chunk, PLp floats starting at the tile's first padded
-// row land at buf + im*img_lds + cl*PLp. Every lane moves 16 bytes per
-// instruction (buffer_load_dwordx4 ... lds). Copies may run past the tile's rows
-// into the channel's LDS padding; the buffer range stops them at the end of the
-// input tensor (such lanes read 0).
+// and each channel of the chunk, the channel's LDS slot of PLp floats at
+// buf + im*img_lds + cl*PLp.
 //
-// zero_outside: with an unpadded input, also store zeros over the image
-// columns of the rows outside the image (their border), for buffers that may
-// hold another tile's rows from an earlier copy.
+// Padded input: PLp floats starting at the tile's first padded row, every lane
+// moving 16 bytes per instruction (buffer_load_dwordx4 ... lds). Copies may run
+// past the tile's rows into the slot's padding; the buffer range stops them at
+// the end of the input tensor (such lanes read 0).
+//
+// Unpadded input: the chunk's slots are rewritten whole, each instruction
+// filling one block of consecutive LDS floats (64 lanes of 16 or 4 bytes)
+// whatever the row length. A lane maps its LDS position to (slot cl, staged
+// row i, column x of the image row y = in_row0 + i - pad) and takes the image
+// pixels there; everything else (border columns, rows outside the image, the
+// pitch gap, the slot's tail) reads as zeros through an offset past the
+// buffer's range. So no border survives from an earlier tile, and no separate
+// zero fill is needed. With dma16 (W and the row starts 16-byte aligned,
+// pitch and shift + pad multiples of 4) a lane's four floats lie all inside or
+// all outside the image row; otherwise each lane moves one.
 __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__restrict__ xp, float *buf, int ch,
-                                               int ig, int in_row0, int wave, int lane, bool zero_outside = false) {
+                                               int ig, int in_row0, int wave, int lane) {
     const int c0 = ch * a.Cc;
     const int cn = min(a.Cc, a.C - c0);
     if (a.unpadded) {
-        // From the unpadded input: padded row in_row0 + i of the tile is image
-        // row y = in_row0 + i - pad; its W floats land at column pad of the
-        // channel's LDS row i, 64 per instruction (one dword per lane, lanes
-        // past the row masked off). Rows outside the image and the border
-        // columns are never written: they keep the zeros the kernel stored
-        // in both buffers before the first copy.
-        // Units are (channel, row) pairs, dealt round-robin to the waves; a
-        // unit copies its row in segments of 64 lanes: 16 bytes per lane when
-        // rows are 16-byte aligned in HBM and LDS (dma16), else 4.
         const int per_lane = a.dma16 ? 4 : 1;
-        const int seg_floats = kWave * per_lane;
-        const int segs = (a.W + seg_floats - 1) / seg_floats;
-        int cl = 0, i = wave;
-        while (i >= a.rows_in) {
-            i -= a.rows_in;
-            ++cl;
-        }
-        for (; cl < cn; ) {
-            const int y = in_row0 + i - a.pad;
-            if (zero_outside && (y < 0 || y >= a.H)) {
-                for (int im = 0; im < a.ipw; ++im) {
-                    if (ig * a.ipw + im >= a.N) break;
-                    float *dst = buf + im * a.img_lds + cl * a.PLp + a.lds_shift + i * a.vp + a.pad;
-                    for (int x = lane; x < a.W; x += kWave) dst[x] = 0.0f;
+        const int blk_floats = kWave * per_lane;
+        const int span = cn * a.PLp;
+        const int nblk = (span + blk_floats - 1) / blk_floats;
+        // Image rows [y_lo, y_lo + y_span) hold every pixel the tile reads.
+        const int y_lo = max(in_row0 - a.pad, 0);
+        const int y_span = max(min(in_row0 - a.pad + a.rows_in, a.H) - y_lo, 0);
+        // Bytes from the chunk's first row to the end of its last: every image
+        // pixel a lane reads lies below, and `nrec` itself reads as zeros.
+        const uint32_t nrec = (uint32_t)(((size_t)(cn - 1) * a.H + y_span) * a.W * sizeof(float));
+        const int lead = a.lds_shift + a.pad;  // slot position of image column 0, staged row 0
+        for (int im = 0; im < a.ipw; ++im) {
+            const int nn = ig * a.ipw + im;
+            if (nn >= a.N) break;
+            const float *base = xp + (((size_t)nn * a.C + c0) * a.H + y_lo) * a.W;
+            __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, (int)nrec, 0x00020000);
+            float *dst = buf + im * a.img_lds;
+            for (int b = wave; b < nblk; b += kS1Waves) {
+                const int P = b * blk_floats + lane * per_lane;
+                if (P < span) {
+                    const int cl = (int)fast_div((uint32_t)P, a.plp_magic, a.plp_shift);
+                    // t = i*vp + x from image column 0 of staged row 0; t + vp >= 0
+                    // (positions before it belong to row -1, at x >= W).
+                    const int t = P - cl * a.PLp - lead;
+                    const int i = (int)fast_div((uint32_t)(t + a.vp), a.vp_magic, a.vp_shift) - 1;
+                    const int x = t - i * a.vp;
+                    const int y = in_row0 + i - a.pad;
+                    const bool in = i < a.rows_in && x < a.W && y >= 0 && y < a.H;  // x >= 0 and i >= 0 follow
+                    const uint32_t voff =
+                        in ? (uint32_t)((cl * a.H + (y - y_lo)) * a.W + x) * (uint32_t)sizeof(float) : nrec;
+                    if (a.dma16)
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(dst + b * blk_floats), 16, voff, 0,
+                                                                 0, 0);
+                    else
+                        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(dst + b * blk_floats), 4, voff, 0,
+                                                                 0, 0);
                 }
-            }
-            if (y >= 0 && y < a.H) {
-                for (int im = 0; im < a.ipw; ++im) {
-                    const int nn = ig * a.ipw + im;
-                    if (nn >= a.N) break;
-                    const float *src = xp + (((size_t)nn * a.C + c0 + cl) * a.H + y) * a.W;
-                    float *dst = buf + im * a.img_lds + cl * a.PLp + a.lds_shift + i * a.vp + a.pad;
-                    for (int sg = 0; sg < segs; ++sg) {
-                        const int x0 = sg * seg_floats;
-                        if (lane * per_lane < a.W - x0) {
-                            if (a.dma16) {
-                                __amdgpu_buffer_rsrc_t rsrc =
-                                    __builtin_amdgcn_make_buffer_rsrc((void *)(src + x0), (short)0, (a.W - x0) * 4,
-                                                                      0x00020000);
-                                __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(dst + x0), 16, lane * 16,
-                                                                         0, 0, 0);
-                            } else {
-                                __builtin_amdgcn_global_load_lds((global_void_t *)(src + x0 + lane),
-                                                                 (lds_void_t *)(dst + x0), 4, 0, 0);
-                            }
-                        }
-                    }
-                }
-            }
-            i += kS1Waves;
-            while (i >= a.rows_in) {
-                i -= a.rows_in;
-                ++cl;
             }
         }
         return;
@@ -1214,15 +1209,8 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
         return r;
     };
     if (b >= T) return;
-    if (a.unpadded) {
-        // The border columns of both buffers stay zero for every tile (no copy
-        // writes them); rows outside the image are zeroed by each staging.
-        for (int e = (int)threadIdx.x * 4; e < 2 * a.buf_floats; e += kS1Threads * 4)
-            *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        __syncthreads();
-    }
     Item cur = item_of(0);
-    stage_chunk_s1(a, xp, lds, 0, cur.ig, cur.ty * a.TH, wave, lane, PERSIST);
+    stage_chunk_s1(a, xp, lds, 0, cur.ig, cur.ty * a.TH, wave, lane);
     wait_async_copies();
     __syncthreads();
     int sbuf = 0;  // buffer of the chunk being computed
@@ -1251,9 +1239,9 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
             const bool more = ch + 1 < a.nchunks;
             float *nbuf = lds + (sbuf ^ 1) * a.buf_floats;
             if (more)
-                stage_chunk_s1(a, xp, nbuf, ch + 1, cur.ig, y0, wave, lane, PERSIST);
+                stage_chunk_s1(a, xp, nbuf, ch + 1, cur.ig, y0, wave, lane);
             else if ((!POOL || a.pool_in_buf) && has_next)
-                stage_chunk_s1(a, xp, nbuf, 0, nxt.ig, nxt.ty * a.TH, wave, lane, PERSIST);
+                stage_chunk_s1(a, xp, nbuf, 0, nxt.ig, nxt.ty * a.TH, wave, lane);
             // Entry lists of this chunk, clamped to the stream.
             int st[RPW], ne[RPW], no[RPW];
             int total = 0, done = 0;
@@ -1301,17 +1289,9 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
             __syncthreads();
         } else if constexpr (POOL) {
             // The staging tile overlaps the buffers: the next tile's first
-            // chunk is copied after every wave's pooled stores. With an
-            // unpadded input the staging also overwrote border positions that
-            // no copy rewrites: they are zeroed again first.
+            // chunk is copied after every wave's pooled stores.
             __syncthreads();
-            if (a.unpadded) {
-                const int staged = kS1Waves * IPW * kWave * PI;
-                for (int e = (int)threadIdx.x * 4; e < staged; e += kS1Threads * 4)
-                    *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-                __syncthreads();
-            }
-            stage_chunk_s1(a, xp, lds + sbuf * a.buf_floats, 0, nxt.ig, nxt.ty * a.TH, wave, lane, true);
+            stage_chunk_s1(a, xp, lds + sbuf * a.buf_floats, 0, nxt.ig, nxt.ty * a.TH, wave, lane);
             wait_async_copies();
             __syncthreads();
         }
@@ -1403,13 +1383,6 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
 
     Window<kCompact> win[RPW];
     RawWindow next[RPW];
-    if (a.unpadded) {
-        // Zero both chunk buffers once: the staging of an unpadded input never
-        // writes the border positions, which must read as the zero padding.
-        for (int e = (int)threadIdx.x * 4; e < 2 * a.buf_floats; e += kS1Threads * 4)
-            *reinterpret_cast<float4 *>(lds + e) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-        __syncthreads();
-    }
     stage_chunk_s1(a, xp, lds, 0, ig, y0, wave, lane);
 #pragma unroll
     for (int i = 0; i < RPW; ++i) {
@@ -2168,16 +2141,17 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.buf_floats = pl.buf_floats;
     if (pl.kind == Kind::kStride1 && pool) {
         // Pair-maxima staging needs an even pitch; it fits the buffer of the
-        // last chunk when 16 waves x IPW images x 64 lanes x PI/2 maxima do
-        // (and the input is padded: an unpadded input's buffers keep border
-        // zeros that no copy rewrites, which the staging would overwrite).
+        // last chunk when 16 waves x IPW images x 64 lanes x PI/2 maxima do.
         a.pool_pairs = (a.vp % 2 == 0) ? 1 : 0;
-        a.pool_in_buf = (a.pool_pairs && !unpadded &&
+        a.pool_in_buf = (a.pool_pairs &&
                          (long long)kS1Waves * pl.IPW * kWave * (pl.PI / 2) <= (long long)pl.buf_floats)
                             ? 1
                             : 0;
     }
     a.PLp = pl.PLp;
+    a.plp_magic = 1;
+    a.plp_shift = 0;
+    if (pl.kind == Kind::kStride1 && !div_magic((uint32_t)pl.PLp, &a.plp_magic, &a.plp_shift)) return SPCONV_EINVAL;
     a.total_floats = (size_t)N * C * Hp * Wp;
     a.wv = pl.wv;
     a.total_wgs = pl.total_wgs;
