@@ -529,12 +529,17 @@ class SparseConvLayer:
             self._lowered_cache[key] = t
         return self._lowered_cache[key]
 
-    # The kernels stage an unpadded input one image row per LDS-DMA instruction,
-    # and on MI355X such a copy costs about the same per instruction up to 1
-    # KiB; rows narrower than this many bytes make the copies slower than a
-    # separate pad pass (measured: 224-byte rows 3.4x the time of 1 KiB
-    # copies for the same bytes, 896-byte rows on par).
+    # The dense kernel stages an unpadded input one image row per LDS-DMA
+    # instruction, and on MI355X such a copy costs about the same per
+    # instruction up to 1 KiB; rows narrower than this many bytes make the
+    # copies slower than a separate pad pass (measured: 224-byte rows 3.4x the
+    # time of 1 KiB copies for the same bytes, 896-byte rows on par).
     MIN_ROW_BYTES_PAD_IN_KERNEL = 768
+    # The stride-1 sparse kernel fills whole 1 KiB LDS blocks per instruction
+    # whatever the row length, 16 bytes per lane when the rows are whole 16-byte
+    # groups: then forming the border costs less than a pad pass (measured at
+    # 16x16, 28x28, 56x56, 224x224). With 4 bytes per lane (W not a multiple
+    # of 4) the two cost about the same (14x14), and the pad pass is kept.
 
     def can_pad_in_kernel(self, N: int) -> bool:
         """Whether this layer's kernel can form the zero border itself (the
@@ -546,8 +551,13 @@ class SparseConvLayer:
 
     def pads_in_kernel(self, N: int) -> bool:
         """Whether ``forward`` forms the zero border in the kernel (it can, and
-        the rows are wide enough for that to beat a pad pass)."""
-        return self.can_pad_in_kernel(N) and 4 * self.W >= self.MIN_ROW_BYTES_PAD_IN_KERNEL
+        that beats a pad pass: rows of whole 16-byte groups for the sparse
+        stride-1 kernel, wide enough rows for the dense kernel)."""
+        if not self.can_pad_in_kernel(N):
+            return False
+        if self.path == "dense":
+            return 4 * self.W >= self.MIN_ROW_BYTES_PAD_IN_KERNEL
+        return self.W % 4 == 0
 
     def forward(self, x, out=None, stream=None, out_pad: int = 0, residual=None, residual_pad: int = 0, xp=None,
                 pad_in_kernel: bool | None = None):
