@@ -474,7 +474,7 @@ def per_config_record(name, args, dev, stream):
         nbytes -= 4.0 * N * C * ((H + 2 * layer.pad) * (W + 2 * layer.pad) - H * W)
     rec = {"workload": name, "description": WORKLOADS[name], "path": L.path, "nnz": nnz,
            "density": round(nnz / (K * C * R * S), 5), "pad": "in the kernel" if fused_pad else "separate pass",
-           "plan": L.plan(N),
+           "plan": L.plan(N, unpadded=fused_pad),
            "ms_per_layer": round(ms_cold, 5), "ms_per_layer_warm": round(ms_warm, 5),
            "ms_per_layer_with_pad": round(ms_step_cold, 5),
            "nonzero_gflops": round(flops / (ms_cold * 1e-3) / 1e9, 1),
@@ -570,7 +570,7 @@ def bench_vgg(args, dev):
     in_kernel = L1.pads_in_kernel(N)
     if not in_kernel:
         L1.pad_input(xd, out=xp, stream=stream)
-    plans = [L1.plan(N), L2.plan(N)]
+    plans = [L1.plan(N, unpadded=in_kernel), L2.plan(N)]
     print(f"[bench] plans {plans}, layer 1 pads in the kernel: {in_kernel}", file=sys.stderr, flush=True)
 
     def conv1():
@@ -748,7 +748,7 @@ def main():
                                layer.pool, device=dev, path=args.path, N=N)
     nnz = L.host_csr.nnz
     dense = L.path == "dense"
-    print(f"[bench] path {L.path}: {L.plan(N)}", file=sys.stderr, flush=True)
+    print(f"[bench] path {L.path}: {L.plan(N, unpadded=L.pads_in_kernel(N))}", file=sys.stderr, flush=True)
     x = torch.from_numpy(layer.x).to(dev)
     xp = torch.empty((N, C, H + 2 * layer.pad, W + 2 * layer.pad), dtype=torch.float32, device=dev)
     out = torch.empty((N, K, L.Ho, L.Wo), dtype=torch.float32, device=dev)

@@ -579,14 +579,18 @@ class SparseConvLayer:
         return self.forward_padded(xp, out=out, stream=stream, out_pad=out_pad, residual=residual,
                                    residual_pad=residual_pad)
 
-    def plan(self, N: int) -> dict:
+    def plan(self, N: int, unpadded: bool = False) -> dict:
+        """The launch plan of a forward of batch N: on the padded input, or with
+        ``unpadded`` on the unpadded one (the kernel forming the border, as
+        ``forward`` does when ``pads_in_kernel``), whose LDS row pitch may differ."""
+        flags = self.flags | (SPCONV_UNPADDED_INPUT if unpadded else 0)
         if self.path == "dense":
-            return spconv_dense_plan(N, self.C, self.H, self.W, self.K, self.R, self.S, self.pad, self.flags)
+            return spconv_dense_plan(N, self.C, self.H, self.W, self.K, self.R, self.S, self.pad, flags)
         lw = self.path == "sparse" and self.use_lowered and spconv_plan(
             N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride, self.pad,
-            self.flags)["kernel"] == SPCONV_KERNEL_STRIDE1
+            flags)["kernel"] == SPCONV_KERNEL_STRIDE1
         return spconv_plan(N, self.C, self.H, self.W, self.csr, self.K, self.R, self.S, self.stride, self.pad,
-                           self.flags, lowered=lw)
+                           flags, lowered=lw)
 
     def run(self, x, xp=None, out=None, stream=None):
         xp = self.pad_input(x, out=xp, stream=stream)
