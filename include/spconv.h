@@ -274,8 +274,10 @@ int spconv_lowered_size(int N, int C, int H, int W, const spconv_csr *csr, int K
  * memory here: rowptr, colidx and vals are read (offset is not), and checked
  * to be a valid CSR of a (K, C*R*S) matrix (rowptr starts at 0, does not
  * decrease and ends at nnz; colidx strictly increasing within a row and below
- * C*R*S). Output channels are assigned to the waves of each channel tile as
- * the kernel would pair them (ranked by entry count, dealt in snake order).
+ * C*R*S). Output channels are assigned to the (wave, slot) pairs of each
+ * channel tile so that the waves' entries are even within every chunk: ranked
+ * by entry count and dealt in snake order, then refined by swaps of rows
+ * between waves (deterministic); the header's k names each slot's channel.
  * lowered  host array of capacity int32 words; spconv_lowered_size words are
  *          written.
  * Errors: as spconv_lowered_size; SPCONV_EINVAL for a NULL lowered or an

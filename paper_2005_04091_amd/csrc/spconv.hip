@@ -2334,6 +2334,83 @@ extern "C" int spconv_lowered_size(int N, int C, int H, int W, const spconv_csr 
     return SPCONV_OK;
 }
 
+namespace {
+
+// Refines the assignment of a channel tile's rows to (wave, slot) so that the
+// waves' work is even within every chunk, not only over the whole row: the
+// workgroup waits at each chunk's barrier for its busiest SIMD (waves w,
+// w+4, w+8, w+12 share one), and a SIMD whose work sits in one wave finishes
+// late too (a lone wave issues at about half the SIMD's rate). Cost of a
+// chunk: the largest over SIMDs of max(SIMD entries, 2 x its largest wave's
+// entries); the assignment takes the best swap of two rows of different waves
+// while that lowers the sum over chunks (deterministic, a bounded number of
+// passes). slot_row[w*RPW + i] is a row (k >= K: an empty slot).
+void balance_slots(std::vector<int> &slot_row, const int32_t *rp, const int32_t *ci, int K, int RS, int Cc,
+                   int nchunks, int RPW) {
+    const int KT = (int)slot_row.size();
+    constexpr int kSimds = 4;
+    // Entries of each slot's row per chunk.
+    std::vector<int> cnt((size_t)KT * nchunks, 0);
+    for (int q = 0; q < KT; ++q) {
+        const int k = slot_row[q];
+        if (k >= K) continue;
+        for (int j = rp[k]; j < rp[k + 1]; ++j) ++cnt[(size_t)q * nchunks + (ci[j] / RS) / Cc];
+    }
+    std::vector<int> wl((size_t)kS1Waves * nchunks, 0);  // wave loads
+    for (int q = 0; q < KT; ++q)
+        for (int c = 0; c < nchunks; ++c) wl[(size_t)(q / RPW) * nchunks + c] += cnt[(size_t)q * nchunks + c];
+    auto chunk_cost = [&](int c) {
+        long long worst = 0;
+        for (int sm = 0; sm < kSimds; ++sm) {
+            long long sum = 0, top = 0;
+            for (int w = sm; w < kS1Waves; w += kSimds) {
+                const long long v = wl[(size_t)w * nchunks + c];
+                sum += v;
+                top = std::max(top, v);
+            }
+            worst = std::max(worst, std::max(sum, 2 * top));
+        }
+        return worst;
+    };
+    auto total = [&]() {
+        long long t = 0;
+        for (int c = 0; c < nchunks; ++c) t += chunk_cost(c);
+        return t;
+    };
+    auto swap_rows = [&](int a, int b) {
+        const int wa = a / RPW, wb = b / RPW;
+        for (int c = 0; c < nchunks; ++c) {
+            const int da = cnt[(size_t)a * nchunks + c], db = cnt[(size_t)b * nchunks + c];
+            wl[(size_t)wa * nchunks + c] += db - da;
+            wl[(size_t)wb * nchunks + c] += da - db;
+            std::swap(cnt[(size_t)a * nchunks + c], cnt[(size_t)b * nchunks + c]);
+        }
+        std::swap(slot_row[a], slot_row[b]);
+    };
+    long long cur = total();
+    for (int pass = 0; pass < 64; ++pass) {
+        long long best = cur;
+        int ba = -1, bb = -1;
+        for (int a = 0; a < KT; ++a)
+            for (int b = a + 1; b < KT; ++b) {
+                if (a / RPW == b / RPW) continue;
+                swap_rows(a, b);
+                const long long t = total();
+                swap_rows(a, b);
+                if (t < best) {
+                    best = t;
+                    ba = a;
+                    bb = b;
+                }
+            }
+        if (ba < 0) break;
+        swap_rows(ba, bb);
+        cur = best;
+    }
+}
+
+}  // namespace
+
 extern "C" int spconv_pack_lowered(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride,
                                    int pad, uint32_t flags, const spconv_options *opt, int32_t *lowered,
                                    int64_t capacity) {
@@ -2367,8 +2444,8 @@ extern "C" int spconv_pack_lowered(int N, int C, int H, int W, const spconv_csr 
         const int k0 = kt * KT;
         // Rows of this channel tile by entry count, most first (ties: lower
         // channel first), dealt to (slot i, wave w) in snake order: ranks
-        // i*16 + w for even i, i*16 + 15 - w for odd i. One row per wave
-        // needs no ranking.
+        // i*16 + w for even i, i*16 + 15 - w for odd i (one row per wave
+        // needs no ranking); then balanced chunk by chunk (balance_slots).
         for (int j = 0; j < KT; ++j) order[j] = j;
         auto nz = [&](int j) { return k0 + j < K ? rp[k0 + j + 1] - rp[k0 + j] : -1; };
         if (pl.RPW > 1)
@@ -2377,6 +2454,7 @@ extern "C" int spconv_pack_lowered(int N, int C, int H, int W, const spconv_csr 
             const int i = r / kS1Waves, w = (i & 1) ? kS1Waves - 1 - r % kS1Waves : r % kS1Waves;
             slot_row[w * pl.RPW + i] = k0 + order[r];
         }
+        balance_slots(slot_row, rp, ci, K, R * S, pl.Cc, pl.nchunks, pl.RPW);
         for (int w = 0; w < kS1Waves; ++w)
             for (int i = 0; i < pl.RPW; ++i) {
                 const int k = slot_row[w * pl.RPW + i];

@@ -2,8 +2,10 @@
 
 ``spconv_pack_lowered`` is compared word for word with an independent numpy
 construction of the layout include/spconv.h documents (headers per (tile, wave,
-slot, chunk), rows ranked by entry count and dealt in snake order, entries
-re-based to the plan's staged tile and split by tap parity), over layers whose
+slot, chunk), entries re-based to the plan's staged tile and split by tap
+parity), given the packer's assignment of rows to (wave, slot), which is
+checked to cover each channel tile's rows once and to balance the chunks' work
+no worse than the snake deal by entry count it starts from, over layers whose
 plans cover one, two and four rows per wave, one and several chunks, several
 images per tile, pooling and the unpadded-input tile geometry; its errors and
 the forward call's checks of a stream are exercised with never-dereferenced
@@ -23,8 +25,44 @@ def sp():
     return spconv
 
 
-def reference_stream(host, plan, K, C, R, S):
-    """The documented layout, built directly from the CSR arrays."""
+def snake_slots(host, K, kt, rpw):
+    """The snake deal by entry count that the packer starts from: {(wave, slot): row}."""
+    rp = host.rowptr
+    kt_rows = 16 * rpw
+    k0 = kt * kt_rows
+    nz = [int(rp[k0 + j + 1] - rp[k0 + j]) if k0 + j < K else -1 for j in range(kt_rows)]
+    order = sorted(range(kt_rows), key=lambda j: (-nz[j], j)) if rpw > 1 else list(range(kt_rows))
+    slot = {}
+    for rank, j in enumerate(order):
+        i, w = divmod(rank, 16)
+        slot[(15 - w if i % 2 else w, i)] = k0 + j
+    return slot
+
+
+def chunk_costs(host, plan, K, C, R, S, slots):
+    """Sum over chunks of the busiest SIMD's cost, max(SIMD entries, 2 x its
+    largest wave's entries), for one channel tile's {(wave, slot): row}."""
+    rp, ci = host.rowptr, host.colidx
+    cc, nch = plan["channels_per_chunk"], plan["chunks"]
+    load = np.zeros((16, nch), np.int64)
+    for (w, i), k in slots.items():
+        if k < K:
+            for j in range(rp[k], rp[k + 1]):
+                load[w, (int(ci[j]) // (R * S)) // cc] += 1
+    per_simd = load.reshape(4, 4, nch)   # wave w = 4 * g + s runs on SIMD s
+    return int(np.maximum(per_simd.sum(axis=0), 2 * per_simd.max(axis=0)).max(axis=0).sum())
+
+
+def packed_slots(got, plan, K, kt):
+    """{(wave, slot): row} of one channel tile, read from the stream's headers (chunk 0)."""
+    rpw, nch = plan["channels_per_wave"], plan["chunks"]
+    hdr = got[:4 * (-(-K // (16 * rpw))) * 16 * rpw * nch].reshape(-1, 16, rpw, nch, 4)
+    return {(w, i): int(hdr[kt, w, i, 0, 3]) for w in range(16) for i in range(rpw)}
+
+
+def reference_stream(host, plan, K, C, R, S, assign):
+    """The documented layout, built directly from the CSR arrays for the
+    given (wave, slot) -> row assignment of each channel tile."""
     rpw, cc, nch = plan["channels_per_wave"], plan["channels_per_chunk"], plan["chunks"]
     plp, vp, shift = plan["lds_channel_floats"], plan["lds_row_pitch"], plan["lds_col_shift"]
     kt_rows = 16 * rpw
@@ -33,12 +71,7 @@ def reference_stream(host, plan, K, C, R, S):
     headers, entries = [], []
     for kt in range(nkt):
         k0 = kt * kt_rows
-        nz = [int(rp[k0 + j + 1] - rp[k0 + j]) if k0 + j < K else -1 for j in range(kt_rows)]
-        order = sorted(range(kt_rows), key=lambda j: (-nz[j], j)) if rpw > 1 else list(range(kt_rows))
-        slot = {}
-        for rank, j in enumerate(order):
-            i, w = divmod(rank, 16)
-            slot[(15 - w if i % 2 else w, i)] = k0 + j
+        slot = assign[kt]
         for w in range(16):
             for i in range(rpw):
                 k = slot[(w, i)]
@@ -86,7 +119,18 @@ def test_stream_matches_documented_layout(sp, case):
     plan = sp.spconv_plan(N, C, H, W, sp.host_csr_struct(host), K, 3, 3, 1, 1, flags, max_row_nnz=mx)
     assert plan["kernel"] == sp.SPCONV_KERNEL_STRIDE1
     got = sp.spconv_pack_lowered(host, N, H, W, 1, 1, flags, mx)
-    ref = reference_stream(host, plan, K, C, 3, 3)
+    nkt = -(-K // (16 * plan["channels_per_wave"]))
+    assign = [packed_slots(got, plan, K, kt) for kt in range(nkt)]
+    for kt, slots in enumerate(assign):
+        # every row of the tile in exactly one slot, the tile's padding rows empty (k = K)
+        k0, kt_rows = kt * 16 * plan["channels_per_wave"], 16 * plan["channels_per_wave"]
+        rows = sorted(slots.values())
+        want = sorted(k if k < K else K for k in range(k0, k0 + kt_rows))
+        assert rows == want
+        # the balancing never does worse than the snake deal it starts from
+        snake = {ws: (k if k < K else K) for ws, k in snake_slots(host, K, kt, plan["channels_per_wave"]).items()}
+        assert chunk_costs(host, plan, K, C, 3, 3, slots) <= chunk_costs(host, plan, K, C, 3, 3, snake)
+    ref = reference_stream(host, plan, K, C, 3, 3, assign)
     assert got.shape == ref.shape
     assert np.array_equal(got, ref)
     nh = -(-K // (16 * plan["channels_per_wave"])) * 16 * plan["channels_per_wave"] * plan["chunks"]
