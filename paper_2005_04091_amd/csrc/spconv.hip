@@ -1732,8 +1732,9 @@ FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool, int mode = kModePlain) {
 // control), and the 16 waves of a workgroup share one LDS. Each chunk adds a
 // fixed cost (barrier, pipeline refill) and the LDS writes of its copy, halo
 // rows included; the pooled epilogue adds a staging round (LDS writes and
-// the 2x2 reductions) per channel of a wave. Workgroups run one per CU, in
-// rounds of 256.
+// the 2x2 reductions) per channel of a wave, 4000 cycles since it stages pair
+// maxima (at 8000 the model picked (22,1,1) for the 224x224 pooled layer,
+// 0.5-2.5% slower than (16,1,2)). Workgroups run one per CU, in rounds of 256.
 // Uneven nonzero counts between the waves of a workgroup cost little while
 // the slowest wave has at most ~1.3x the mean (the others' LDS bandwidth
 // passes to it as they finish). Beyond that the workgroup waits for it: with
@@ -1802,7 +1803,7 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho
         if (floats > (size_t)kS1LdsFloats) return;
         const double compute = kS1Waves * RPW * row_nnz * 2.0 * (IPW * PI + 1.0) * imb;
         const double wg_cycles =
-            compute + nchunks * (3000.0 + IPW * (double)Cc * PLp / 32.0) + (pool ? 8000.0 * RPW : 0.0);
+            compute + nchunks * (3000.0 + IPW * (double)Cc * PLp / 32.0) + (pool ? 4000.0 * RPW : 0.0);
         const double time = (double)ceil_div((int)std::min<long long>(wgs, 1 << 30), 256) * wg_cycles;
         if (best_time < 0 || time < best_time * 0.999) {
             best_time = time;
