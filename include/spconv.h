@@ -320,13 +320,21 @@ typedef struct spconv_plan_info {
      * on a tiling of SPCONV_KERNEL_STRIDE1_TILED with more than 256 work
      * items, 256 workgroups (one per CU) that take the work items in turn. */
     int32_t launch_workgroups;
+    /* Stride-1 kernel with a lowered stream (opt->lowered non-NULL), unpooled,
+     * one image per tile: virtual pixels per row-spanning tile. Tile t of an
+     * image then covers its virtual pixels [t * tile_pixels, (t+1) *
+     * tile_pixels) (pixel y*lds_row_pitch + x), starting in any column, and
+     * tile_rows is the most output rows such a tile touches. 0: tiles of
+     * tile_rows whole rows. */
+    int32_t tile_pixels;
 } spconv_plan_info;
 
 /*
  * spconv_plan - the launch plan spconv_forward_ex would use for these arguments
  * (host only, queues nothing). Takes the same arguments as spconv_forward_ex
- * without the buffers and applies the same checks (opt nullable; only its
- * max_row_nnz steers the plan); csr's arrays are not read. Meant for tests,
+ * without the buffers and applies the same checks (opt nullable; its
+ * max_row_nnz steers the plan, and whether lowered is non-NULL selects the
+ * lowered-stream launch, whose tiles may span rows); csr's arrays are not read. Meant for tests,
  * tools and reports that need to know which kernel variant and tiling run.
  * Errors: those of spconv_forward_ex's argument checks; SPCONV_EINVAL for a
  * NULL info.

@@ -640,6 +640,7 @@ extern "C" int spconv_dense_plan(int N, int C, int H, int W, int K, int R, int S
     info->lds_bytes = (int64_t)pl.lds_bytes;
     info->lds_channel_floats = info->lds_row_pitch = info->lds_col_shift = 0;
     info->launch_workgroups = pl.total_wgs;
+    info->tile_pixels = 0;
     return SPCONV_OK;
 }
 

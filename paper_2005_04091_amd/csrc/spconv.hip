@@ -447,6 +447,10 @@ struct FwdArgs {
     // pooled epilogue: the pitch vp is even, so pixel pairs are horizontal
     // pool pairs (pair-maxima staging), and that staging fits one chunk buffer
     int pool_pairs, pool_in_buf;
+    // stride-1 kernel with a lowered stream: virtual pixels per row-spanning
+    // tile (tile t covers [t*span, (t+1)*span) of its image, from the row it
+    // starts in), or 0 for tiles of TH whole rows
+    int span;
 };
 
 // Entries fetched per scalar load in the lowered walk (one s_load_dwordx16),
@@ -491,12 +495,13 @@ constexpr int kStageBlock = 256;     // floats per 16-byte-per-lane LDS DMA inst
 
 // Queue the asynchronous copy of one channel chunk: for each image of the group
 // and each channel of the chunk, the channel's LDS slot of PLp floats at
-// buf + im*img_lds + cl*PLp.
+// buf + im*img_lds + cl*PLp. The slot starts at column col0 of padded row
+// in_row0 (col0 = 0 but for the window of a row-spanning tile).
 //
-// Padded input: PLp floats starting at the tile's first padded row, every lane
-// moving 16 bytes per instruction (buffer_load_dwordx4 ... lds). Copies may run
-// past the tile's rows into the slot's padding; the buffer range stops them at
-// the end of the input tensor (such lanes read 0).
+// Padded input: PLp consecutive floats from there, every lane moving 16 bytes
+// per instruction (buffer_load_dwordx4 ... lds). Copies may run past the
+// tile's rows into the slot's padding; the buffer range stops them at the end
+// of the input tensor (such lanes read 0).
 //
 // Unpadded input: the chunk's slots are rewritten whole, each instruction
 // filling one block of consecutive LDS floats (64 lanes of 16 or 4 bytes)
@@ -509,7 +514,7 @@ constexpr int kStageBlock = 256;     // floats per 16-byte-per-lane LDS DMA inst
 // pitch and shift + pad multiples of 4) a lane's four floats lie all inside or
 // all outside the image row; otherwise each lane moves one.
 __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__restrict__ xp, float *buf, int ch,
-                                               int ig, int in_row0, int wave, int lane) {
+                                               int ig, int in_row0, int wave, int lane, int col0 = 0) {
     const int c0 = ch * a.Cc;
     const int cn = min(a.Cc, a.C - c0);
     if (a.unpadded) {
@@ -536,7 +541,7 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
                     const int cl = (int)fast_div((uint32_t)P, a.plp_magic, a.plp_shift);
                     // t = i*vp + x from image column 0 of staged row 0; t + vp >= 0
                     // (positions before it belong to row -1, at x >= W).
-                    const int t = P - cl * a.PLp - lead;
+                    const int t = P - cl * a.PLp - lead + col0;
                     const int i = (int)fast_div((uint32_t)(t + a.vp), a.vp_magic, a.vp_shift) - 1;
                     const int x = t - i * a.vp;
                     const int y = in_row0 + i - a.pad;
@@ -559,7 +564,7 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
     for (int im = 0; im < a.ipw; ++im) {
         const int nn = ig * a.ipw + im;
         if (nn >= a.N) break;
-        const size_t first = ((size_t)(nn * a.C + c0) * a.Hp + in_row0) * a.Wp;
+        const size_t first = ((size_t)(nn * a.C + c0) * a.Hp + in_row0) * a.Wp + col0;
         const size_t avail = (a.total_floats - first) * sizeof(float);
         const int nrec = avail > 0xffffffffull ? (int)0xffffffffu : (int)(uint32_t)avail;
         __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void *)(xp + first), (short)0, nrec, 0x00020000);
@@ -953,7 +958,7 @@ constexpr int lowered_pipeline_buffers() {
 template <int PI, int IPW, int RPW, bool POOL>
 __device__ __forceinline__ void s1_epilogue(const FwdArgs &a, float2 (&accE)[RPW][IPW][PI / 2],
                                             float2 (&accO)[RPW][IPW][PI / 2], const int (&krow)[RPW], int ig, int ty,
-                                            int y0, int wave, int lane, float *lds, float *stage,
+                                            int y0, int phi, int wave, int lane, float *lds, float *stage,
                                             const float *__restrict__ bias, const float *__restrict__ res,
                                             float *__restrict__ out) {
     constexpr int PJ = PI / 2;
@@ -961,16 +966,20 @@ __device__ __forceinline__ void s1_epilogue(const FwdArgs &a, float2 (&accE)[RPW
     const int tile_px = a.TH * a.vp;
     if constexpr (!POOL) {
         // Tile row of each of this lane's pixels, or -1 when the pixel is not
-        // stored. Pixel qq = yl*vp + x of the tile lands at qq + yl*(pitch - vp)
-        // past the tile's first element, in the output and the residual alike.
+        // stored (outside the output, or past a row-spanning tile's span). The
+        // tile starts at column phi of row y0 (0 for whole-row tiles): tile
+        // pixel qq is pixel qa = qq + phi = yl*vp + x counted from row y0, and
+        // lands at qa + yl*(pitch - vp) past that row's first element, in the
+        // output and the residual alike.
+        const int span = a.span ? a.span : tile_px;
         int ylo[PJ][2];
 #pragma unroll
         for (int p = 0; p < PJ; ++p)
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const int qq = q + 2 * kWave * p + h;
-                const int yl = (int)fast_div((uint32_t)qq, a.vp_magic, a.vp_shift), x = qq - yl * a.vp;
-                ylo[p][h] = (qq < tile_px && x < a.Wo && y0 + yl < a.Ho) ? yl : -1;
+                const int qq = q + 2 * kWave * p + h, qa = qq + phi;
+                const int yl = (int)fast_div((uint32_t)qa, a.vp_magic, a.vp_shift), x = qa - yl * a.vp;
+                ylo[p][h] = (qq < span && x < a.Wo && y0 + yl < a.Ho) ? yl : -1;
             }
         const int odelta = a.opitch - a.vp, rdelta = a.rpitch - a.vp;
 #pragma unroll
@@ -994,7 +1003,7 @@ __device__ __forceinline__ void s1_epilogue(const FwdArgs &a, float2 (&accE)[RPW
                     for (int p = 0; p < PJ; ++p) {
                         const int yl = ylo[p][0];
                         if (yl < 0) continue;
-                        const int qq = q + 2 * kWave * p;
+                        const int qq = q + 2 * kWave * p + phi;
                         float2 v = make_float2(sum[p].x + bk, sum[p].y + bk);
                         if (rp) {
                             const f32x2_a4_t r = *reinterpret_cast<const f32x2_a4_t *>(rp + qq + yl * rdelta);
@@ -1014,16 +1023,26 @@ __device__ __forceinline__ void s1_epilogue(const FwdArgs &a, float2 (&accE)[RPW
                     for (int h = 0; h < 2; ++h) {
                         const int yl = ylo[p][h];
                         if (yl < 0) continue;
-                        const int qq = q + 2 * kWave * p + h;
+                        const int qq = q + 2 * kWave * p + h + phi;
                         float v = (h ? sum[p].y : sum[p].x) + bk;
                         if (rp) v += rp[qq + yl * rdelta];
                         if (a.relu) v = v > 0.0f ? v : 0.0f;
                         store_out(op + qq + yl * odelta, v, a.out_pad == 0);
                     }
                 }
-                if (a.out_pad)
-                    zero_border(plane, y0, min(y0 + a.TH, a.Ho), a.Ho, a.Wo, a.out_pad, a.opitch, ty == 0,
+                if (a.out_pad) {
+                    // The side borders of the rows whose column 0 lies in this
+                    // tile (its whole rows: rows y0 .. y0 + TH - 1).
+                    int r0 = y0, r1 = min(y0 + a.TH, a.Ho);
+                    if (a.span) {
+                        r0 = y0 + (phi > 0 ? 1 : 0);
+                        r1 = min((int)fast_div((uint32_t)(y0 * a.vp + phi + a.span + a.vp - 1), a.vp_magic,
+                                               a.vp_shift),
+                                 a.Ho);
+                    }
+                    zero_border(plane, r0, max(r0, r1), a.Ho, a.Wo, a.out_pad, a.opitch, ty == 0,
                                 ty == a.ntiles_y - 1, lane, kWave);
+                }
             }
         }
     } else if (a.pool_pairs) {
@@ -1196,6 +1215,13 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
     struct Item {
         int kt, ty, ig;
     };
+    // First output row of tile ty (= first staged padded input row). A
+    // row-spanning tile starts at column phi of that row and stages the window
+    // from column phi rounded down to a multiple of 4.
+    auto row0_of = [&](int ty) {
+        return a.span ? (int)fast_div((uint32_t)(ty * a.span), a.vp_magic, a.vp_shift) : ty * a.TH;
+    };
+    auto col0_of = [&](int ty, int row0) { return a.span ? (ty * a.span - row0 * a.vp) & ~3 : 0; };
     // Round it holds items it*G .. min((it+1)*G, T) - 1; workgroup b takes
     // the one at its XCD-ordered position among that round's (b is below
     // the round's size whenever the round has an item for it).
@@ -1210,14 +1236,20 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
     };
     if (b >= T) return;
     Item cur = item_of(0);
-    stage_chunk_s1(a, xp, lds, 0, cur.ig, cur.ty * a.TH, wave, lane);
+    {
+        const int r0 = row0_of(cur.ty);
+        stage_chunk_s1(a, xp, lds, 0, cur.ig, r0, wave, lane, col0_of(cur.ty, r0));
+    }
     wait_async_copies();
     __syncthreads();
     int sbuf = 0;  // buffer of the chunk being computed
     for (int it = 0;; ++it) {
         const bool has_next = PERSIST && (it + 1) * G + b < T;
         const Item nxt = has_next ? item_of(it + 1) : cur;
-        const int y0 = cur.ty * a.TH;
+        const int y0 = row0_of(cur.ty);
+        const int phi = a.span ? cur.ty * a.span - y0 * a.vp : 0;
+        const int col0 = phi & ~3;
+        const int nrow0 = row0_of(nxt.ty), ncol0 = col0_of(nxt.ty, nrow0);
         int krow[RPW];
         int4 h[RPW];
 #pragma unroll
@@ -1239,9 +1271,9 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
             const bool more = ch + 1 < a.nchunks;
             float *nbuf = lds + (sbuf ^ 1) * a.buf_floats;
             if (more)
-                stage_chunk_s1(a, xp, nbuf, ch + 1, cur.ig, y0, wave, lane);
+                stage_chunk_s1(a, xp, nbuf, ch + 1, cur.ig, y0, wave, lane, col0);
             else if ((!POOL || a.pool_in_buf) && has_next)
-                stage_chunk_s1(a, xp, nbuf, 0, nxt.ig, nxt.ty * a.TH, wave, lane);
+                stage_chunk_s1(a, xp, nbuf, 0, nxt.ig, nrow0, wave, lane, ncol0);
             // Entry lists of this chunk, clamped to the stream.
             int st[RPW], ne[RPW], no[RPW];
             int total = 0, done = 0;
@@ -1252,7 +1284,8 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
                 no[i] = min(max(h[i].z, 0), a.lw_entries - st[i] - ne[i]);
                 total += ne[i] + no[i];
             }
-            const int qv = sbuf * a.buf_floats + q;
+            // The window starts col0 before the tile's first pixel.
+            const int qv = sbuf * a.buf_floats + q + (phi - col0);
             set_progress_prio(0, total);
 #pragma unroll
             for (int i = 0; i < RPW; ++i) {
@@ -1279,8 +1312,8 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
         // The pooled staging goes to the buffer of the last chunk (now free)
         // when it fits there, else over both buffers.
         float *stage = (POOL && a.pool_in_buf) ? lds + (sbuf ^ 1) * a.buf_floats : lds;
-        s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, cur.ig, cur.ty, y0, wave, lane, lds, stage, bias, res,
-                                        out);
+        s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, cur.ig, cur.ty, y0, phi, wave, lane, lds, stage, bias,
+                                        res, out);
         if (!has_next) break;
         if (POOL && a.pool_in_buf) {
             // The next tile's first chunk is in the other buffer; its second
@@ -1291,7 +1324,7 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
             // The staging tile overlaps the buffers: the next tile's first
             // chunk is copied after every wave's pooled stores.
             __syncthreads();
-            stage_chunk_s1(a, xp, lds + sbuf * a.buf_floats, 0, nxt.ig, nxt.ty * a.TH, wave, lane);
+            stage_chunk_s1(a, xp, lds + sbuf * a.buf_floats, 0, nxt.ig, nrow0, wave, lane, ncol0);
             wait_async_copies();
             __syncthreads();
         }
@@ -1453,7 +1486,7 @@ __global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(4, 4
         }
     }
 
-    s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, ig, ty, y0, wave, lane, lds, lds, bias, res, out);
+    s1_epilogue<PI, IPW, RPW, POOL>(a, accE, accO, krow, ig, ty, y0, 0, wave, lane, lds, lds, bias, res, out);
 }
 
 // Generic-stride kernel: waves split the pixels of the tile and every wave
@@ -1648,6 +1681,7 @@ struct Plan {
     int P = 0, KT = 0;             // generic kernel
     int TH = 0, ntiles_y = 0, ipw = 0, wpi = 0, Cc = 0, nchunks = 0, rows_in = 0, PL = 0, PLp = 0, img_lds = 0;
     int buf_floats = 0, wv = 0, rows_per_wg = 0, nktiles = 0, total_wgs = 0;
+    int span = 0;  // stride-1 kernel: virtual pixels per row-spanning tile (0: tiles of TH whole rows)
     size_t lds_bytes = 0;
 };
 
@@ -1747,20 +1781,42 @@ FwdKernel pick_s1(int PI, int IPW, int RPW, bool pool, int mode = kModePlain) {
 // layers, so that the model orders each layer's tilings as measured.
 // vp: pitch of the virtual tile and of the staged LDS rows; shift: LDS column
 // of padded column 0 (both Wp and 0 for a padded input).
+// span_ok: the chosen tiling's tiles of one image may also be row-spanning:
+// tile t covers the virtual pixels [t*span, (t+1)*span) of the image, span =
+// 64*PI - 2, whatever rows they fall in, so no lane computes pixels of rows a
+// whole-row tile would have to leave out (at 224x224 with PI = 16, 4 rows of
+// 228 fill 912 of a tile's 1024 pixels). Unpooled layers with a lowered stream
+// only (224x224 layer: 56 -> 50 tiles per image, 636 -> 615 us).
 bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho, int Wo, int R, int S, bool pool,
-                  long long nnz, long long max_row_nnz, Plan *out) {
+                  long long nnz, long long max_row_nnz, bool span_ok, Plan *out) {
     const int img_pix = Ho * vp;
     const double row_nnz = std::max(1.0, (double)nnz / K);
     const double skew = max_row_nnz > 0 ? (double)max_row_nnz / row_nnz : 1.0;
     Plan best;
     double best_time = -1.0;
-    auto consider = [&](int PI, int IPW, int RPW) {
+    auto consider = [&](int PI, int IPW, int RPW, bool spanning) {
         if (!pick_s1(PI, IPW, RPW, pool)) return;
         // Virtual pixels per image tile. The last one (64*PI - 1) has no odd-tap
         // partner, so a tile holds at most cap - 1 pixels.
         const int cap = kWave * PI;
-        int TH, nt;
-        if (img_pix <= cap - 1) {
+        int TH, nt, span = 0;
+        if (spanning) {
+            // Row-spanning tiles of span (even) pixels up to the last stored
+            // one; TH = the most output rows a tile touches.
+            // The lanes' pixel pairs stay aligned only if every tile starts at
+            // an even column: span and the pitch even.
+            if (IPW != 1 || img_pix <= cap - 1 || (vp & 1)) return;
+            span = cap - 2;
+            const long long last = (long long)(Ho - 1) * vp + Wo;
+            nt = (int)((last + span - 1) / span);
+            TH = 0;
+            for (int t = 0; t < nt; ++t) {
+                const long long s0 = (long long)t * span;
+                const int r0 = (int)(s0 / vp);
+                const int r1 = (int)std::min<long long>((s0 + span - 1) / vp, Ho - 1);
+                TH = std::max(TH, r1 - r0 + 1);
+            }
+        } else if (img_pix <= cap - 1) {
             TH = Ho;
             nt = 1;
         } else {
@@ -1773,17 +1829,28 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho
             if (pool && (TH & 1)) ++TH;
             nt = ceil_div(Ho, TH);
         }
-        const int rows_in = TH + R - 1;
-        const int PL = rows_in * vp + shift;
+        int rows_in = TH + R - 1;
+        int PL = rows_in * vp + shift;
+        if (spanning) {
+            // A row-spanning tile stages only the window of virtual pixels it
+            // reads: from its first pixel's column rounded down to a multiple
+            // of 4 (col0, at most 3 before it) through its last lane's last
+            // tap, so the window holds cap + (R-1)*vp + S pixels and a little
+            // more, however the tile sits in its rows. rows_in = the most rows
+            // such a window touches.
+            PL = shift + 3 + cap + (R - 1) * vp + S;
+            rows_in = ceil_div(vp + PL, vp);
+        }
         // Channel slots 16-byte aligned; a slot's last copy masks the lanes
         // past it (rounding slots up to whole 256-float copies would cost
         // LDS and, at 64 channels of 56x56, a fourth chunk).
         const int PLp = ceil_div(PL, 4) * 4;
-        // Lanes past the tile read up to cap - TH*vp + S - 2 floats beyond the
-        // last image block (values that only dropped pixels use). Past the
-        // first buffer they land in the second; past the second, in one slack
-        // area after it.
-        const int slack = cap - TH * vp + S;
+        // Lanes past a whole-row tile read up to cap - TH*vp + S - 2 floats
+        // beyond the last image block (values that only dropped pixels use).
+        // Past the first buffer they land in the second; past the second, in
+        // one slack area after it. A row-spanning tile's window holds every
+        // read of its lanes.
+        const int slack = spanning ? S : cap - TH * vp + S;
         int cc_max = ((kS1LdsFloats - slack) / 2) / (IPW * PLp);
         if (cc_max < 1) return;
         cc_max = std::min(cc_max, C);
@@ -1825,16 +1892,21 @@ bool plan_stride1(int N, int C, int K, int Hp, int Wp, int vp, int shift, int Ho
             best.rows_per_wg = KT;
             best.nktiles = ceil_div(K, KT);
             best.total_wgs = (int)wgs;
+            best.span = span;
             best.lds_bytes = floats * sizeof(float);
         }
     };
     for (int RPW : {1, 2, 4}) {
-        for (int PI : kPiSingle) consider(PI, 1, RPW);
+        for (int PI : kPiSingle) consider(PI, 1, RPW, false);
         for (int IPW : {2, 4})
             if (IPW <= N)
-                for (int PI : kPiMulti) consider(PI, IPW, RPW);
+                for (int PI : kPiMulti) consider(PI, IPW, RPW, false);
     }
     if (best_time < 0) return false;
+    // Row-spanning tiles are a choice of geometry for the chosen tiling, made
+    // when they are modelled faster, so that a layer runs the same kernel
+    // instance with or without a lowered stream.
+    if (span_ok && !pool && best.IPW == 1) consider(best.PI, 1, best.RPW, true);
     *out = best;
     return true;
 }
@@ -2060,7 +2132,7 @@ namespace {
 // Host-side checks of a forward call (everything but the buffer pointers) and
 // its launch plan. Returns SPCONV_OK or SPCONV_EINVAL.
 int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, int R, int S, int stride, int pad,
-                    uint32_t flags, long long max_row_nnz, Plan *plp, FwdArgs *ap) {
+                    uint32_t flags, long long max_row_nnz, bool lowered, Plan *plp, FwdArgs *ap) {
     if (!csr) return SPCONV_EINVAL;
     if (N < 1 || C < 1 || H < 1 || W < 1 || K < 1 || R < 1 || S < 1 || stride < 1 || pad < 0) return SPCONV_EINVAL;
     if (flags & ~(SPCONV_RELU | SPCONV_MAXPOOL2X2 | SPCONV_UNPADDED_INPUT)) return SPCONV_EINVAL;
@@ -2090,10 +2162,11 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     } else {
         if (row16)
             ok = plan_stride1(N, C, K, (int)Hp, (int)Wp, ((int)Wp + 3) / 4 * 4, (4 - pad % 4) % 4, Ho, Wo, R, S,
-                              pool, csr->nnz, max_row_nnz, &pl);
+                              pool, csr->nnz, max_row_nnz, lowered, &pl);
         if (!ok) {
             row16 = false;
-            ok = plan_stride1(N, C, K, (int)Hp, (int)Wp, (int)Wp, 0, Ho, Wo, R, S, pool, csr->nnz, max_row_nnz, &pl);
+            ok = plan_stride1(N, C, K, (int)Hp, (int)Wp, (int)Wp, 0, Ho, Wo, R, S, pool, csr->nnz, max_row_nnz,
+                              lowered, &pl);
         }
     }
     if (!ok) return SPCONV_EINVAL;
@@ -2106,6 +2179,7 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.pair_store = 0;
     a.lw_headers = a.lw_entries = 0;
     a.pool_pairs = a.pool_in_buf = 0;
+    a.span = pl.kind == Kind::kStride1 ? pl.span : 0;
     if (!div_magic((uint32_t)Wp, &a.wp_magic, &a.wp_shift)) return SPCONV_EINVAL;
     if (!div_magic((uint32_t)a.vp, &a.vp_magic, &a.vp_shift)) return SPCONV_EINVAL;
     a.H = H;
@@ -2221,7 +2295,8 @@ extern "C" int spconv_forward_ex(const float *in_padded, int N, int C, int H, in
     if (!in_padded || !out) return SPCONV_EINVAL;
     Plan pl;
     FwdArgs a;
-    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, &pl, &a);
+    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0,
+                             opt && opt->lowered, &pl, &a);
     if (rc != SPCONV_OK) return rc;
     rc = apply_epilogue(opt, &a);
     if (rc != SPCONV_OK) return rc;
@@ -2267,7 +2342,8 @@ extern "C" int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, in
     if (!info) return SPCONV_EINVAL;
     Plan pl;
     FwdArgs a;
-    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, &pl, &a);
+    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0,
+                             opt && opt->lowered, &pl, &a);
     if (rc != SPCONV_OK) return rc;
     rc = apply_epilogue(opt, &a);
     if (rc != SPCONV_OK) return rc;
@@ -2288,6 +2364,7 @@ extern "C" int spconv_plan(int N, int C, int H, int W, const spconv_csr *csr, in
     info->lds_col_shift = s1 ? a.lds_shift : 0;
     info->launch_workgroups =
         launch_grid(pl, launch_mode(pl, opt && opt->lowered, (flags & SPCONV_MAXPOOL2X2) != 0));
+    info->tile_pixels = s1 ? pl.span : 0;
     return SPCONV_OK;
 }
 
@@ -2324,7 +2401,8 @@ extern "C" int spconv_lowered_size(int N, int C, int H, int W, const spconv_csr 
     if (!words) return SPCONV_EINVAL;
     Plan pl;
     FwdArgs a;
-    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, &pl, &a);
+    int rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, true, &pl,
+                             &a);
     if (rc != SPCONV_OK) return rc;
     rc = apply_epilogue(opt, &a);
     if (rc != SPCONV_OK) return rc;
@@ -2421,7 +2499,8 @@ extern "C" int spconv_pack_lowered(int N, int C, int H, int W, const spconv_csr 
     if (rc != SPCONV_OK) return rc;
     Plan pl;
     FwdArgs a;
-    rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, &pl, &a);
+    rc = prepare_forward(N, C, H, W, csr, K, R, S, stride, pad, flags, opt ? opt->max_row_nnz : 0, true, &pl,
+                             &a);
     if (rc != SPCONV_OK) return rc;
     // The CSR, read on the host: a valid (K, C*R*S) matrix.
     const long long nnz = csr->nnz, cols = (long long)C * R * S;

@@ -58,7 +58,8 @@ class spconv_plan_info(ctypes.Structure):
                 ("tiles_per_image", ctypes.c_int32), ("channels_per_chunk", ctypes.c_int32),
                 ("chunks", ctypes.c_int32), ("workgroups", ctypes.c_int32), ("threads_per_workgroup", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int64), ("lds_channel_floats", ctypes.c_int32), ("lds_row_pitch", ctypes.c_int32),
-                ("lds_col_shift", ctypes.c_int32), ("launch_workgroups", ctypes.c_int32)]
+                ("lds_col_shift", ctypes.c_int32), ("launch_workgroups", ctypes.c_int32),
+                ("tile_pixels", ctypes.c_int32)]
 
 
 _c_int = ctypes.c_int

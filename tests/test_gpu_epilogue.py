@@ -191,3 +191,36 @@ def test_resnet_basic_block(sp):
     check_close(y1, r1, a1, "block conv1")
     r2, a2 = oracle.conv(np.ascontiguousarray(y1), l2.w, l2.mask, l2.bias, 1, 1, True, False, residual=x)
     check_close(y2.cpu().numpy(), r2, a2, "block conv2 + shortcut")
+
+
+def test_row_spanning_tiles_with_residual_and_border(sp):
+    """A 224x224 layer of 32 images plans row-spanning tiles with a lowered
+    stream (tiles of 64*PI - 2 virtual pixels starting in any column) and
+    whole-row tiles without one: with a residual read from a bordered tensor
+    and a bordered output, the two launches give the same bits, and both the
+    oracle's values inside an all-zero border."""
+    import torch
+    layer = synth.random_layer(8900, 32, 32, 64, 224, 224, density=0.2)
+    N, C, H, W, K, R, S = layer.shape
+    say("row-spanning tiles", layer.shape)
+    rng = np.random.default_rng(8901)
+    res = rng.uniform(-1, 1, (N, K, H, W)).astype(np.float32)
+    resp = np.pad(res, ((0, 0), (0, 0), (1, 1), (1, 1)))
+    outs = {}
+    for lowered in (False, True):
+        L = sp.SparseConvLayer(layer.w, layer.mask, layer.bias, H, W, 1, 1, True, False, lowered=lowered)
+        plan = L.plan(N)
+        assert (plan["tile_pixels"] > 0) == lowered, plan
+        xd = torch.from_numpy(layer.x).cuda()
+        xp = L.pad_input(xd)
+        out = torch.full((N, K, H + 2, W + 2), float("nan"), device="cuda")
+        L.forward_padded(xp, out=out, out_pad=1, residual=torch.from_numpy(resp).cuda(), residual_pad=1)
+        torch.cuda.synchronize()
+        outs[lowered] = out.cpu().numpy()
+    assert np.array_equal(outs[False].view(np.uint32), outs[True].view(np.uint32))
+    o = outs[True]
+    border = np.ones(o.shape[2:], bool)
+    border[1:-1, 1:-1] = False
+    assert np.all(o[:, :, border].view(np.uint32) == 0)
+    ref, ab = oracle.conv(layer.x, layer.w, layer.mask, layer.bias, 1, 1, True, False, residual=res)
+    check_close(o[:, :, 1:-1, 1:-1], ref, ab, "row-spanning tiles")

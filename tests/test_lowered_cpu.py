@@ -245,3 +245,80 @@ def test_persistent_schedule_takes_every_item_once(T):
             seen.append(t * G + _xcd_linear_id(b, min(G, T - t * G)))
             t += 1
     assert sorted(seen) == list(range(T))
+
+
+def _spanning_geometry_ok(Ho, Wo, vp, shift, R, S, PI, span, nt, PLp):
+    """Row-spanning tiles as the stride-1 kernel indexes them: tile t starts at
+    virtual pixel t*span of its image (row0 = that // vp, column phi), stages
+    the window from column phi & ~3 of row0, and its lanes (64*PI tile pixels
+    from phi) read window index (phi - col0) + q + r*vp + s + shift. Checks
+    that the tiles' stored pixels are each output pixel once, that every read
+    of every lane stays in [0, PLp), and that the rows whose column 0 falls in
+    a tile (the side borders it zeroes) partition the rows."""
+    cap = 64 * PI
+    seen = np.zeros((Ho, Wo), np.int32)
+    border_rows = np.zeros(Ho, np.int32)
+    for t in range(nt):
+        s0 = t * span
+        row0 = s0 // vp
+        phi = s0 - row0 * vp
+        col0 = phi & ~3
+        assert phi % 2 == 0 and (phi - col0) in (0, 2)
+        q = np.arange(span)
+        qa = q + phi
+        y, x = row0 + qa // vp, qa % vp
+        ok = (x < Wo) & (y < Ho)
+        np.add.at(seen, (y[ok], x[ok]), 1)
+        # the lowest read is an entry index (>= 0, odd taps stored rounded
+        # down) plus phi - col0 >= 0; the highest the last lane's last tap
+        hi = (phi - col0) + cap - 1 + (R - 1) * vp + (S - 1) + shift
+        assert phi - col0 >= 0 and hi < PLp, (t, hi, PLp)
+        r0 = row0 + (1 if phi > 0 else 0)
+        r1 = min(-(-(row0 * vp + phi + span) // vp), Ho)
+        border_rows[r0:max(r0, r1)] += 1
+    assert np.all(seen == 1)
+    assert np.all(border_rows == 1)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_spanning_tiles_cover_each_pixel_once(seed):
+    rng = np.random.default_rng(9300 + seed)
+    for _ in range(60):
+        PI = int(rng.choice([8, 12, 14, 16, 20, 24]))
+        Wo = int(rng.integers(8, 300))
+        Ho = int(rng.integers(2, 80))
+        vp = Wo + 2 + int(rng.integers(0, 3))
+        vp += vp & 1                                   # the planner requires an even pitch
+        shift = int(rng.choice([0, 1, 2, 3]))
+        span = 64 * PI - 2
+        if Ho * vp <= 64 * PI - 1:
+            continue                                   # whole-image tiles
+        nt = -(-((Ho - 1) * vp + Wo) // span)
+        PLp = -(-(shift + 3 + 64 * PI + 2 * vp + 3) // 4) * 4
+        _spanning_geometry_ok(Ho, Wo, vp, shift, 3, 3, PI, span, nt, PLp)
+
+
+def test_vgg_layer_plans_spanning_tiles_with_a_stream_only(sp):
+    layer = synth.random_layer(9400, 32, 64, 64, 224, 224, density=0.2)
+    host = sp.spconv_pack_csr(layer.w, layer.mask, 226, 226)
+    st = sp.host_csr_struct(host)
+    mx = int(np.diff(host.rowptr).max())
+    for flags in (sp.flags_of(True, False), sp.flags_of(True, False) | sp.SPCONV_UNPADDED_INPUT):
+        p = sp.spconv_plan(32, 64, 224, 224, st, 64, 3, 3, 1, 1, flags, max_row_nnz=mx, lowered=True)
+        plain = sp.spconv_plan(32, 64, 224, 224, st, 64, 3, 3, 1, 1, flags, max_row_nnz=mx)
+        assert plain["tile_pixels"] == 0
+        assert (p["pixels_per_lane"], p["channels_per_wave"]) == (plain["pixels_per_lane"], plain["channels_per_wave"])
+        span, vp = p["tile_pixels"], p["lds_row_pitch"]
+        assert span == 64 * p["pixels_per_lane"] - 2
+        assert p["tiles_per_image"] == -(-(223 * vp + 224) // span)
+        _spanning_geometry_ok(224, 224, vp, p["lds_col_shift"], 3, 3, p["pixels_per_lane"], span,
+                              p["tiles_per_image"], p["lds_channel_floats"])
+        # the stream for this plan, word for word
+        got = sp.spconv_pack_lowered(host, 32, 224, 224, 1, 1, flags, mx)
+        nkt = -(-64 // (16 * p["channels_per_wave"]))
+        assign = [packed_slots(got, p, 64, kt) for kt in range(nkt)]
+        assert np.array_equal(got, reference_stream(host, p, 64, 64, 3, 3, assign))
+    # pooled layers keep whole-row tiles
+    pooled = sp.spconv_plan(32, 64, 224, 224, st, 64, 3, 3, 1, 1, sp.flags_of(True, True), max_row_nnz=mx,
+                            lowered=True)
+    assert pooled["tile_pixels"] == 0
