@@ -39,9 +39,13 @@ def snake_slots(host, K, kt, rpw):
     return slot
 
 
+AGE_SHARE = np.array([120, 107, 93, 80], np.int64)  # issue share of wave 4*g + s, by age group g
+
+
 def chunk_costs(host, plan, K, C, R, S, slots):
-    """Sum over chunks of the busiest SIMD's cost, max(SIMD entries, 2 x its
-    largest wave's entries), for one channel tile's {(wave, slot): row}."""
+    """Sum over chunks of the busiest SIMD's cost, max(SIMD entries, each of
+    its waves' entries scaled by the wave's age share), for one channel tile's
+    {(wave, slot): row}."""
     rp, ci = host.rowptr, host.colidx
     cc, nch = plan["channels_per_chunk"], plan["chunks"]
     load = np.zeros((16, nch), np.int64)
@@ -50,7 +54,8 @@ def chunk_costs(host, plan, K, C, R, S, slots):
             for j in range(rp[k], rp[k + 1]):
                 load[w, (int(ci[j]) // (R * S)) // cc] += 1
     per_simd = load.reshape(4, 4, nch)   # wave w = 4 * g + s runs on SIMD s
-    return int(np.maximum(per_simd.sum(axis=0), 2 * per_simd.max(axis=0)).max(axis=0).sum())
+    scaled = per_simd * AGE_SHARE.sum() * 1000 // AGE_SHARE[:, None, None]
+    return int(np.maximum(per_simd.sum(axis=0) * 1000, scaled.max(axis=0)).max(axis=0).sum())
 
 
 def packed_slots(got, plan, K, kt):
