@@ -1269,11 +1269,20 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
                 }
         for (int ch = 0; ch < a.nchunks; ++ch) {
             const bool more = ch + 1 < a.nchunks;
+            // The copy of the next chunk (or of the next tile's first). The
+            // oldest wave of each SIMD issues its share before its walk, the
+            // other three halfway through their lists (after the first row's
+            // two lists, or after the even list of a single row): issued all
+            // at once, some 80 one-KiB copies queue at the CU's texture path
+            // and hold the younger waves up to 2 us at the issue; spread this
+            // way the copy still lands well before the chunk ends.
             float *nbuf = lds + (sbuf ^ 1) * a.buf_floats;
-            if (more)
-                stage_chunk_s1(a, xp, nbuf, ch + 1, cur.ig, y0, wave, lane, col0);
-            else if ((!POOL || a.pool_in_buf) && has_next)
-                stage_chunk_s1(a, xp, nbuf, 0, nxt.ig, nrow0, wave, lane, ncol0);
+            const bool do_stage = more || ((!POOL || a.pool_in_buf) && has_next);
+            const int s_ch = more ? ch + 1 : 0, s_ig = more ? cur.ig : nxt.ig;
+            const int s_row = more ? y0 : nrow0, s_col = more ? col0 : ncol0;
+            constexpr int kLateList = RPW > 1 ? 2 : 1;  // list before which the younger waves issue
+            const bool early = wave < 4;  // wave w runs on SIMD w % 4, and waves 0..3 are the oldest
+            if (do_stage && early) stage_chunk_s1(a, xp, nbuf, s_ch, s_ig, s_row, wave, lane, s_col);
             // Entry lists of this chunk, clamped to the stream.
             int st[RPW], ne[RPW], no[RPW];
             int total = 0, done = 0;
@@ -1291,9 +1300,13 @@ __device__ __forceinline__ void s1_lowered_tiles(const FwdArgs &a, const float *
             for (int i = 0; i < RPW; ++i) {
                 run_lowered<NBL>(accE[i], ent, st[i], ne[i], lds, qv, a.img_lds);
                 done += ne[i];
+                if (2 * i + 1 == kLateList && do_stage && !early)
+                    stage_chunk_s1(a, xp, nbuf, s_ch, s_ig, s_row, wave, lane, s_col);
                 set_progress_prio(done, total);
                 run_lowered<NBL>(accO[i], ent, st[i] + ne[i], no[i], lds, qv, a.img_lds);
                 done += no[i];
+                if (2 * i + 2 == kLateList && do_stage && !early)
+                    stage_chunk_s1(a, xp, nbuf, s_ch, s_ig, s_row, wave, lane, s_col);
                 set_progress_prio(done, total);
             }
             if (more) {
