@@ -327,3 +327,46 @@ def test_vgg_layer_plans_spanning_tiles_with_a_stream_only(sp):
     pooled = sp.spconv_plan(32, 64, 224, 224, st, 64, 3, 3, 1, 1, sp.flags_of(True, True), max_row_nnz=mx,
                             lowered=True)
     assert pooled["tile_pixels"] == 0
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"c{c[0]}" for c in CASES])
+def test_plans_reserve_the_prefetch_sink(sp, case):
+    # The walk's entry-stream prefetch lands in 64 floats after everything else
+    # the stride-1 kernel keeps in LDS: the plan's dynamic LDS must hold the two
+    # chunk buffers (or the pooled staging) plus that sink, within 160 KiB.
+    seed, N, C, K, H, W, pool, d, skew, unpadded = case
+    layer = synth.random_layer(7000 + seed, N, C, K, H, W, density=d, pool=pool, skew=skew)
+    host = sp.spconv_pack_csr(layer.w, layer.mask, H + 2, W + 2)
+    flags = sp.flags_of(True, pool) | (sp.SPCONV_UNPADDED_INPUT if unpadded else 0)
+    for lowered in (False, True):
+        p = sp.spconv_plan(N, C, H, W, sp.host_csr_struct(host), K, 3, 3, 1, 1, flags,
+                           max_row_nnz=int(np.diff(host.rowptr).max()), lowered=lowered)
+        assert p["kernel"] == sp.SPCONV_KERNEL_STRIDE1
+        buf = -(-p["images_per_group"] * p["channels_per_chunk"] * p["lds_channel_floats"] // 64) * 64
+        need = 2 * buf
+        if pool:
+            need = max(need, 16 * p["images_per_group"] * 64 * p["pixels_per_lane"])
+        assert p["lds_bytes"] >= 4 * (need + 64)
+        assert p["lds_bytes"] <= 160 * 1024
+
+
+def test_packer_gives_older_waves_more_entries(sp):
+    # Waves w, w+4, w+8, w+12 share a SIMD, which issues the oldest ready wave
+    # first; the packer weights each wave's entries by its age share, so on a
+    # VGG-shaped layer the oldest quarter of the waves carries more entries per
+    # chunk than the youngest, while each SIMD's total stays balanced.
+    layer = synth.random_layer(9401, 32, 64, 64, 224, 224, density=0.2)
+    host = sp.spconv_pack_csr(layer.w, layer.mask, 226, 226)
+    mx = int(np.diff(host.rowptr).max())
+    flags = sp.flags_of(True, False)
+    p = sp.spconv_plan(32, 64, 224, 224, sp.host_csr_struct(host), 64, 3, 3, 1, 1, flags, max_row_nnz=mx,
+                       lowered=True)
+    got = sp.spconv_pack_lowered(host, 32, 224, 224, 1, 1, flags, mx)
+    rpw, nch = p["channels_per_wave"], p["chunks"]
+    nkt = -(-64 // (16 * rpw))
+    hdr = got[:4 * nkt * 16 * rpw * nch].reshape(nkt, 16, rpw, nch, 4)
+    load = (hdr[..., 1] + hdr[..., 2]).sum(axis=2)          # (tile, wave, chunk)
+    group = load.reshape(nkt, 4, 4, nch).mean(axis=(0, 2, 3))  # by age group (wave // 4)
+    assert group[0] > group[3] * 1.08
+    simd = load.reshape(nkt, 4, 4, nch).sum(axis=1)          # (tile, simd, chunk)
+    assert (simd.max(axis=1) / simd.mean(axis=1)).mean() < 1.08
