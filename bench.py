@@ -19,6 +19,7 @@ record), for profiling.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -738,6 +739,12 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    # No cyclic garbage collection while launches are timed: a full pass over
+    # the interpreter's objects (tens of ms with torch loaded) stalls the host
+    # between two launches and lands inside the events' window (a 47 ms gap
+    # between two back-to-back launches was seen in a kernel trace).
+    gc.collect()
+    gc.disable()
     dev = torch.device("cuda:0")
     if args.workload == "vgg_block" and not args.compare:
         bench_vgg(args, dev)
