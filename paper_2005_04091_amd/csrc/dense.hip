@@ -647,16 +647,28 @@ extern "C" int spconv_dense_plan(int N, int C, int H, int W, int K, int R, int S
 namespace {
 
 // Break-even filter density on MI355X: above it the dense kernel beats the
-// sparse ones. Measured with both paths on the same layers (fp32, batch 32):
-// about 0.24 for 256 channels at 14x14 and about 0.43 for 64 channels at
-// 56x56. The sparse kernels spread each entry's fixed cost over the pixels
-// of an image tile, so their rate, and the break-even, grow with the image:
-// the threshold interpolates log-linearly in pixels per image between those
-// two measurements, clamped to [0.2, 0.5].
+// sparse ones. Measured with both paths on the same layers (fp32, batch 32,
+// back-to-back launches): about 0.245 for 256 channels at 14x14, 0.44 for 128
+// channels at 28x28 with the pool, 0.42-0.47 at 56x56 (64 or 128 channels,
+// pooled or not) and 0.67 for 64 channels at 224x224. The sparse kernels spread
+// each entry's fixed cost over the pixels of an image tile, so their rate,
+// and the break-even, grow with the image: the threshold interpolates
+// log-linearly in output pixels per image between those measurements and
+// stays at the end values beyond them.
 double break_even_density(int Ho, int Wo) {
+    struct Anchor {
+        double px, d;
+    };
+    static constexpr Anchor kAnchors[] = {{196.0, 0.245}, {784.0, 0.44}, {3136.0, 0.43}, {50176.0, 0.67}};
+    constexpr int n = (int)(sizeof(kAnchors) / sizeof(kAnchors[0]));
     const double px = std::max(1.0, (double)Ho * Wo);
-    const double d = 0.24 + (0.43 - 0.24) * std::log2(px / 196.0) / std::log2(3136.0 / 196.0);
-    return std::min(0.5, std::max(0.2, d));
+    if (px <= kAnchors[0].px) return kAnchors[0].d;
+    for (int i = 1; i < n; ++i)
+        if (px <= kAnchors[i].px) {
+            const double t = std::log2(px / kAnchors[i - 1].px) / std::log2(kAnchors[i].px / kAnchors[i - 1].px);
+            return kAnchors[i - 1].d + t * (kAnchors[i].d - kAnchors[i - 1].d);
+        }
+    return kAnchors[n - 1].d;
 }
 
 }  // namespace

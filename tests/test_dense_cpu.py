@@ -116,11 +116,17 @@ def test_select_path(sp):
     assert sel(32, 256, 14, 14, 256, 3, 3, 2, 1, full, 1) == sp.SPCONV_PATH_SPARSE   # stride 2: sparse only
     assert sel(32, 64, 14, 14, 64, 5, 5, 1, 2, 64 * 64 * 25, 1) == sp.SPCONV_PATH_SPARSE  # no 5x5 dense kernel
     assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, 0, 1) == sp.SPCONV_PATH_SPARSE
-    # break-even 0.43 at 56x56, 0.24 at 14x14
+    # measured break-even: 0.43 at 56x56, 0.245 at 14x14, 0.44 at 28x28 (pooled), 0.67 at 224x224
     assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.42 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_SPARSE
     assert sel(32, 64, 56, 56, 64, 3, 3, 1, 1, int(0.44 * 64 * 64 * 9), 1) == sp.SPCONV_PATH_DENSE
     assert sel(32, 256, 14, 14, 256, 3, 3, 1, 1, int(0.23 * full), 1) == sp.SPCONV_PATH_SPARSE
     assert sel(32, 256, 14, 14, 256, 3, 3, 1, 1, int(0.25 * full), 1) == sp.SPCONV_PATH_DENSE
+    c128 = 128 * 128 * 9
+    assert sel(32, 128, 28, 28, 128, 3, 3, 1, 1, int(0.42 * c128), 3) == sp.SPCONV_PATH_SPARSE
+    assert sel(32, 128, 28, 28, 128, 3, 3, 1, 1, int(0.46 * c128), 3) == sp.SPCONV_PATH_DENSE
+    c64 = 64 * 64 * 9
+    assert sel(32, 64, 224, 224, 64, 3, 3, 1, 1, int(0.65 * c64), 1) == sp.SPCONV_PATH_SPARSE
+    assert sel(32, 64, 224, 224, 64, 3, 3, 1, 1, int(0.69 * c64), 1) == sp.SPCONV_PATH_DENSE
     assert sel(32, 64, 224, 224, 64, 3, 3, 1, 1, 64 * 64 * 9, 3) == sp.SPCONV_PATH_SPARSE  # pooled 226-wide rows: no dense plan
     lib, E, out = sp._lib, sp.SPCONV_EINVAL, ctypes.c_int()
     assert lib.spconv_select_path(32, 64, 56, 56, 64, 3, 3, 1, 1, 7280, 1, None) == E
