@@ -77,6 +77,42 @@ inline bool div_magic(uint32_t d, uint32_t *magic, int *shift) {
     return true;
 }
 
+// Work units u = q*n + r (0 <= r < n) dealt round-robin to `step` waves: wave
+// w takes u = w, w + step, ... The staging loops walk (q, r) without a
+// division per unit (a loop of subtractions cost up to step/n scalar
+// iterations per unit, 16 for one-block channel slots). UnitStep holds what
+// that takes for one n: step = dq*n + dr, and recip = ceil(2^16 / n), with
+// which (w * recip) >> 16 = floor(w / n) whenever w*n < 2^16: w*recip / 2^16
+// exceeds w/n by less than w / 2^16 < 1/n, and the fraction of w/n is at
+// most (n-1)/n.
+struct UnitStep {
+    int n, dq, dr;
+    uint32_t recip;
+};
+
+inline bool unit_step(int n, int step, UnitStep *u) {
+    if (n < 1 || step < 1 || (long long)step * n >= 65536) return false;
+    u->n = n;
+    u->dq = step / n;
+    u->dr = step % n;
+    u->recip = (65536u + (uint32_t)n - 1u) / (uint32_t)n;
+    return true;
+}
+
+__device__ __forceinline__ void unit_first(const UnitStep &u, int w, int &q, int &r) {
+    q = (int)(((uint32_t)w * u.recip) >> 16);
+    r = w - q * u.n;
+}
+
+__device__ __forceinline__ void unit_next(const UnitStep &u, int &q, int &r) {
+    q += u.dq;
+    r += u.dr;
+    if (r >= u.n) {
+        r -= u.n;
+        ++q;
+    }
+}
+
 // Raise a kernel instance's dynamic-LDS limit to `bytes` on the current
 // device, once per (device, instance). Every caller of one instance passes
 // the same value (the most any plan of its family uses), so launches of

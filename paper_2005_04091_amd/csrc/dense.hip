@@ -55,6 +55,9 @@ struct DenseArgs {
     int Cc;          // channels per LDS chunk (even)
     int nchunks;
     int PLp;         // LDS floats per staged channel
+    // staging units dealt round-robin to the nw*ks waves: (channel, padded
+    // row) from an unpadded input, (channel, block of kDnsBlock) otherwise
+    UnitStep row_units, blk_units;
     int buf_floats;  // Cc * PLp
     size_t total_floats;  // N*C*Hp*Wp
     int total_wgs;
@@ -90,11 +93,8 @@ __device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__r
         // floats per instruction (lanes past the row masked off). Border rows
         // and columns keep the zeros stored before the first copy.
         const int segs = (a.W + kWave - 1) / kWave;
-        int cl = 0, i = wave;
-        while (i >= a.rows_in) {
-            i -= a.rows_in;
-            ++cl;
-        }
+        int cl, i;
+        unit_first(a.row_units, wave, cl, i);
         while (cl < cn) {
             const int y = row0 + i - a.pad;
             if (y >= 0 && y < a.H) {
@@ -107,36 +107,24 @@ __device__ __forceinline__ void dense_stage(const DenseArgs &a, const float *__r
                                                          4, 0, 0);
                 }
             }
-            i += nwaves;
-            while (i >= a.rows_in) {
-                i -= a.rows_in;
-                ++cl;
-            }
+            unit_next(a.row_units, cl, i);
         }
     }
     if (!a.unpadded) {
-        const int nblk = (a.PLp + kDnsBlock - 1) / kDnsBlock;
         const size_t first = ((size_t)n * a.C + c0) * plane + (size_t)row0 * a.Wp;
         const size_t avail = (a.total_floats - first) * sizeof(float);
         const int nrec = avail > 0xffffffffull ? (int)0xffffffffu : (int)(uint32_t)avail;
         __amdgpu_buffer_rsrc_t rsrc =
             __builtin_amdgcn_make_buffer_rsrc((void *)(xp + first), (short)0, nrec, 0x00020000);
-        int cl = 0, b = wave;
-        while (b >= nblk) {
-            b -= nblk;
-            ++cl;
-        }
+        int cl, b;
+        unit_first(a.blk_units, wave, cl, b);
         while (cl < cn) {
             // Byte offsets of a chunk fit 32 bits (the planner checks).
             const uint32_t voff = (uint32_t)(cl * plane + b * kDnsBlock) * (uint32_t)sizeof(float) + lane * 16;
             if (b * kDnsBlock + lane * 4 < a.PLp)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(buf + cl * a.PLp + b * kDnsBlock), 16,
                                                          voff, 0, 0, 0);
-            b += nwaves;
-            while (b >= nblk) {
-                b -= nblk;
-                ++cl;
-            }
+            unit_next(a.blk_units, cl, b);
         }
     }
     // An odd last chunk reads one channel slot past the tensor's channels with
@@ -581,6 +569,9 @@ int prepare_dense(int N, int C, int H, int W, int K, int R, int S, int pad, uint
     a.Cc = pl.Cc;
     a.nchunks = pl.nchunks;
     a.PLp = pl.PLp;
+    if (!unit_step(a.rows_in, pl.nw * pl.ks, &a.row_units) ||
+        !unit_step((pl.PLp + kDnsBlock - 1) / kDnsBlock, pl.nw * pl.ks, &a.blk_units))
+        return SPCONV_EINVAL;
     a.buf_floats = pl.Cc * pl.PLp;
     a.total_floats = (size_t)N * C * Hp * Wp;
     a.total_wgs = pl.total_wgs;

@@ -402,7 +402,8 @@ struct FwdArgs {
     int rows_in;       // padded input rows staged per tile
     int PL;            // LDS floats per staged channel (rows_in * Wp)
     int img_lds;       // LDS floats per image block (Cc * PL)
-    int PLp;           // LDS pitch of one staged channel (stride-1 kernel: PL rounded up to 256)
+    int PLp;           // LDS pitch of one staged channel (stride-1 kernel: PL rounded up to 4)
+    UnitStep stage_units;  // stride-1 padded staging: (channel, block of kStageBlock) units over 16 waves
     int buf_floats;    // LDS floats per chunk buffer (stride-1 kernel: two buffers)
     size_t total_floats;  // N*C*Hp*Wp, the extent of the padded input
     int wv;            // pixel pitch of the virtual tile: Wp (stride 1) or Wo
@@ -562,7 +563,6 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
         }
         return;
     }
-    const int nblk = (a.PLp + kStageBlock - 1) / kStageBlock;
     const int plane = a.Hp * a.Wp;
     for (int im = 0; im < a.ipw; ++im) {
         const int nn = ig * a.ipw + im;
@@ -573,21 +573,14 @@ __device__ __forceinline__ void stage_chunk_s1(const FwdArgs &a, const float *__
         __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void *)(xp + first), (short)0, nrec, 0x00020000);
         float *dst = buf + im * a.img_lds;
         // Work units (channel cl, block b) are dealt round-robin to the waves.
-        int cl = 0, b = wave;
-        while (b >= nblk) {
-            b -= nblk;
-            ++cl;
-        }
+        int cl, b;
+        unit_first(a.stage_units, wave, cl, b);
         while (cl < cn) {
             const uint32_t voff = (uint32_t)((cl * plane + b * kStageBlock) * (int)sizeof(float)) + lane * 16;
             if (b * kStageBlock + lane * 4 < a.PLp)
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t *)(dst + cl * a.PLp + b * kStageBlock), 16,
                                                          voff, 0, 0, 0);
-            b += kS1Waves;
-            while (b >= nblk) {
-                b -= nblk;
-                ++cl;
-            }
+            unit_next(a.stage_units, cl, b);
         }
     }
 }
@@ -2268,6 +2261,9 @@ int prepare_forward(int N, int C, int H, int W, const spconv_csr *csr, int K, in
     a.plp_magic = 1;
     a.plp_shift = 0;
     if (pl.kind == Kind::kStride1 && !div_magic((uint32_t)pl.PLp, &a.plp_magic, &a.plp_shift)) return SPCONV_EINVAL;
+    a.stage_units = UnitStep{1, kS1Waves, 0, 65536u};
+    if (pl.kind == Kind::kStride1 && !unit_step(ceil_div(pl.PLp, kStageBlock), kS1Waves, &a.stage_units))
+        return SPCONV_EINVAL;
     a.total_floats = (size_t)N * C * Hp * Wp;
     a.wv = pl.wv;
     a.total_wgs = pl.total_wgs;

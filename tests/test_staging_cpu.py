@@ -101,3 +101,32 @@ def test_unpadded_staging_writes_the_padded_layout(seed):
                     want = (c0 + cl, y, x)
             assert got.get(P) == want, (W, H, pad, R, TH, C, Cc, ch, ty, dma16, P)
         done += 1
+
+
+def test_unit_walk_visits_every_unit_once():
+    """The staging loops deal units u = q*n + r to `step` waves without a
+    division per unit: wave w starts at q = (w * ceil(2^16/n)) >> 16, r = w -
+    q*n, and advances by q += step // n, r += step % n with one wrap. For every
+    slot width n a plan can have (channel slots of up to 160 blocks, rows of up
+    to 40) and every wave count, each wave visits exactly u = w, w + step, ..."""
+    for step in (1, 4, 8, 12, 16):
+        for n in range(1, 161):
+            recip = (65536 + n - 1) // n
+            dq, dr = divmod(step, n)
+            total = 7 * n + 3
+            seen = []
+            for w in range(step):
+                q = (w * recip) >> 16
+                r = w - q * n
+                assert (q, r) == divmod(w, n)
+                u = w
+                while q * n + r < total:
+                    assert q * n + r == u and 0 <= r < n
+                    seen.append(u)
+                    q += dq
+                    r += dr
+                    if r >= n:
+                        r -= n
+                        q += 1
+                    u += step
+            assert sorted(seen) == list(range(total))
