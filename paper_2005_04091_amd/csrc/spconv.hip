@@ -830,22 +830,30 @@ __device__ __forceinline__ void run_lowered(float2 (&acc)[IPW][PJ], const int32_
     if (n <= 0) return;
     constexpr int B = kLwBatch;
     static_assert(B % NB == 0, "buffer rotation must repeat every batch");
+    // With few reads per entry (two pixel pairs or fewer), the reads of the
+    // entries after the list's end are issued too, in place of a scalar test
+    // and branch per entry: they are the next lists' entries (or the stream's
+    // zero pad), LDS indices of the same chunk window, and their values are
+    // never used.
+    constexpr bool kEager = IPW * PJ <= 2;
+    // This lane's window base: an entry's address is one shift-add on it.
+    const float *lb = lds + qv;
     f32x2 x[NB][IPW][PJ];
     LwBatch<B> b = *reinterpret_cast<const LwBatch<B> *>(ent + 2 * j);
 #pragma unroll
     for (int u = 0; u < NB - 1; ++u)
-        if (u < n) load_pairs(x[u], lds, b.v[2 * u] + qv, img_lds);
+        if (kEager || u < n) load_pairs(x[u], lb, b.v[2 * u], img_lds);
     int r = n;
     // Main loop, branch free: a whole batch, and the NB - 1 entries whose
     // reads issue ahead of it all exist (the first of them come from the
-    // next batch).
-    for (; r >= B + NB - 1; r -= B) {
+    // next batch), or, eager, are read whether they exist or not.
+    for (; r >= (kEager ? B : B + NB - 1); r -= B) {
         LwBatch<B> nb;
 #pragma unroll
         for (int u = 0; u < B; ++u) {
             if (u == B - NB) nb = *reinterpret_cast<const LwBatch<B> *>(ent + 2 * (j + B));
             const int f = u + NB - 1;  // entry whose reads issue now
-            load_pairs(x[f % NB], lds, (f < B ? b.v[2 * f] : nb.v[2 * (f - B)]) + qv, img_lds);
+            load_pairs(x[f % NB], lb, f < B ? b.v[2 * f] : nb.v[2 * (f - B)], img_lds);
             fma_pairs(acc, x[u % NB], __int_as_float(b.v[2 * u + 1]));
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -863,11 +871,11 @@ __device__ __forceinline__ void run_lowered(float2 (&acc)[IPW][PJ], const int32_
         constexpr int u = decltype(U)::value;
         constexpr int f = u + NB - 1;
         if (u >= r) return false;
-        if (f < r) {
+        if (kEager || f < r) {
             if constexpr (f < B)
-                load_pairs(x[f % NB], lds, b.v[2 * f] + qv, img_lds);
+                load_pairs(x[f % NB], lb, b.v[2 * f], img_lds);
             else
-                load_pairs(x[f % NB], lds, nb.v[2 * (f - B)] + qv, img_lds);
+                load_pairs(x[f % NB], lb, nb.v[2 * (f - B)], img_lds);
         }
         float w;
         if constexpr (u < B)
